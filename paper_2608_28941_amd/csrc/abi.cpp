@@ -1,0 +1,766 @@
+// C ABI and host driver of the range finder (Alg. 2, then explicit Q).
+//
+// Per block i (all on the plan's stream):
+//   panel   (V_i, T_i, tau_i) <- Householder QR of Y_i       (geqrt step)
+//   reduce  Z = V_i^T B[ib:m, :]                              (update step)
+//   formW   W = T_i^T Z
+//   sketch  Omega_{i+1}                                       (sketch step)
+//   update  B[ib:m, :] -= V_i W; Y_{i+1} = B[(i+1)b:m, :] Omega_{i+1};
+//           ||B_i||^2 and ||B[(i+1)b:m, :]||^2                (E step)
+//   final   E, stop flag; the host reads the flag (8 bytes) once per block.
+// Block 0 reads A and writes the workspace, so A itself is never modified.
+// Q = H_0 ... H_{k-1} [I_k; 0] is then formed backward block by block with
+// the same reduce / formW / update kernels (trans = 0).  V, T and tau are
+// binary64 for both dtypes; for float plans Q is accumulated in binary64 and
+// rounded once at the end, because rounding Q to float after each of the s
+// block applications costs about 2 sqrt(s) u sqrt(k) in ||Q^T Q - I||_F.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <type_traits>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "rrf_internal.h"
+
+using namespace rrf;
+
+namespace {
+
+constexpr int kMaxUpdSplits = 8;
+constexpr int kMaxRedSplits = 32;
+constexpr int kOmLd = 64;         // Omega stored [c][q] with row length 64
+constexpr int kTLd = 64;          // T stored like geqrt's T: 64 rows
+
+struct Sizes {
+  int64_t ldb, kcap, kcols;
+  size_t Bws, V, Tm, tau, Ypart, Om, Zpart, W, Q, Q64, normpart, red, rowj,
+      bar, st, trace;
+  size_t total() const {
+    return Bws + V + Tm + tau + Ypart + Om + Zpart + W + Q + Q64 + normpart +
+           red + rowj + bar + st + trace;
+  }
+};
+
+Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
+                    int64_t k_max) {
+  (void)b_max;
+  Sizes z;
+  const size_t e = dt == RRF_F32 ? 4 : 8;
+  z.ldb = round_up(std::max<int64_t>(m_max, 1), 64);
+  z.kcap = std::min(m_max, n_max);
+  if (k_max > 0) z.kcap = std::min(z.kcap, k_max);
+  z.kcols = z.kcap + 64;
+  z.Bws = (size_t)z.ldb * n_max * e;
+  z.V = (size_t)z.ldb * z.kcols * 8;
+  z.Tm = (size_t)kTLd * z.kcols * 8;
+  z.tau = (size_t)z.kcols * 8;
+  z.Ypart = (size_t)kMaxUpdSplits * z.ldb * 64 * e;
+  z.Om = (size_t)n_max * kOmLd * e;
+  z.Zpart = (size_t)kMaxRedSplits * n_max * 64 * 8;
+  z.W = (size_t)n_max * 64 * 8;
+  z.Q = (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * e;
+  z.Q64 = dt == RRF_F32 ? (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * 8 : 0;
+  z.normpart = (size_t)(ceil_div(m_max, kUpdRows) * kMaxUpdSplits + 1) * 2 * 8;
+  z.red = (size_t)2 * kMaxPanelWGs * 64 * 8;
+  z.rowj = (size_t)2 * 64 * 8;
+  z.bar = 256;
+  z.st = sizeof(DevState);
+  z.trace = (size_t)2 * std::max<int64_t>(z.kcap, 1) * 8;
+  return z;
+}
+
+}  // namespace
+
+struct rrf_plan {
+  rrf_dtype dtype;
+  size_t elem;
+  int64_t m_max, n_max, b_max, k_max;
+  hipStream_t stream;
+  int device, num_cus;
+  Sizes sz;
+  std::vector<void*> dev_allocs;
+  void *Bws, *Ypart, *Om, *Zpart, *W, *Q, *Q64;
+  double *V, *Tm, *tau;
+  double *normpart, *red, *rowj, *trace_trail_d, *trace_sub_d;
+  unsigned* bar;
+  DevState* st;
+  DevState* st_host;
+  int stop_mode, timing, panel_target;
+  // last run
+  int64_t last_m, last_n, last_k, last_b, nblocks;
+  double E0, sigma2;
+  std::vector<double> trace_trail, trace_sub;
+  std::vector<int64_t> block_start;
+  double ms[RRF_NUM_STAGES], flops[RRF_NUM_STAGES], bytes[RRF_NUM_STAGES];
+  int64_t launches[RRF_NUM_STAGES];
+  std::vector<hipEvent_t> events;
+  std::vector<int> event_stage;
+  size_t events_used;
+};
+
+namespace {
+
+rrf_status hip_fail(hipError_t e) {
+  if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) return RRF_ERR_NOMEM;
+  return RRF_ERR_HIP;
+}
+
+// RRF_FAULT_ALLOC=N makes the N-th device allocation of a plan fail (tests).
+hipError_t dev_alloc(rrf_plan* p, void** out, size_t bytes, int* counter) {
+  ++*counter;
+  const char* f = std::getenv("RRF_FAULT_ALLOC");
+  if (f && std::atoi(f) == *counter) return hipErrorOutOfMemory;
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMalloc(out, bytes);
+  if (e == hipSuccess) p->dev_allocs.push_back(*out);
+  return e;
+}
+
+void free_plan(rrf_plan* p) {
+  for (void* q : p->dev_allocs) (void)hipFree(q);
+  p->dev_allocs.clear();
+  if (p->st_host) (void)hipHostFree(p->st_host);
+  for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
+  delete p;
+}
+
+int upd_splits(int64_t mr, int64_t n, int num_cus) {
+  const int64_t row_wgs = ceil_div(mr, kUpdRows);
+  int64_t s = ceil_div(4 * (int64_t)num_cus, std::max<int64_t>(row_wgs, 1));
+  s = std::min<int64_t>(s, kMaxUpdSplits);
+  s = std::min<int64_t>(s, std::max<int64_t>(1, n / 256));
+  return (int)std::max<int64_t>(s, 1);
+}
+
+int red_splits(int64_t mr, int64_t n, int num_cus) {
+  const int64_t col_wgs = ceil_div(n, kRedCols);
+  int64_t s = ceil_div(4 * (int64_t)num_cus, std::max<int64_t>(col_wgs, 1));
+  s = std::min<int64_t>(s, kMaxRedSplits);
+  s = std::min<int64_t>(s, std::max<int64_t>(1, mr / 256));
+  return (int)std::max<int64_t>(s, 1);
+}
+
+// ---- timing / statistics --------------------------------------------------
+
+void stats_reset(rrf_plan* p) {
+  for (int i = 0; i < RRF_NUM_STAGES; ++i) {
+    p->ms[i] = p->flops[i] = p->bytes[i] = 0.0;
+    p->launches[i] = 0;
+  }
+  p->events_used = 0;
+  p->event_stage.clear();
+}
+
+hipError_t ev_mark(rrf_plan* p, int stage) {
+  if (!p->timing) return hipSuccess;
+  if (p->events_used == p->events.size()) {
+    hipEvent_t e;
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return r;
+    p->events.push_back(e);
+  }
+  if (p->event_stage.size() < p->events_used + 1) p->event_stage.resize(p->events_used + 1);
+  p->event_stage[p->events_used] = stage;
+  return hipEventRecord(p->events[p->events_used++], p->stream);
+}
+
+// Pairs of events (begin, end) were recorded per launch.
+void stats_collect(rrf_plan* p) {
+  if (!p->timing) return;
+  for (size_t i = 0; i + 1 < p->events_used; i += 2) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p->events[i], p->events[i + 1]) == hipSuccess)
+      p->ms[p->event_stage[i]] += ms;
+  }
+}
+
+#define RRF_LAUNCH(p, stage, fl, by, expr)                 \
+  do {                                                     \
+    hipError_t e_ = ev_mark((p), (stage));                 \
+    if (e_ == hipSuccess) e_ = (expr);                     \
+    if (e_ == hipSuccess) e_ = ev_mark((p), (stage));      \
+    if (e_ != hipSuccess) return hip_fail(e_);             \
+    (p)->launches[stage] += 1;                             \
+    (p)->flops[stage] += (fl);                             \
+    (p)->bytes[stage] += (by);                             \
+  } while (0)
+
+hipError_t read_state(rrf_plan* p) {
+  hipError_t e = hipMemcpyAsync(p->st_host, p->st, sizeof(DevState),
+                                hipMemcpyDeviceToHost, p->stream);
+  if (e != hipSuccess) return e;
+  return hipStreamSynchronize(p->stream);
+}
+
+// X (mr x ncols) <- (I - V T V^T)^T X (trans) or (I - V T V^T) X, with V, T
+// already zero padded to bp columns in plan-compatible layout.
+template <typename T>
+rrf_status apply_wy(rrf_plan* p, int trans, const double* V, int64_t ldv,
+                    const double* Tm, int64_t ldt, int b, int bp, T* X,
+                    int64_t ldx, int64_t mr, int64_t ncols, int stage) {
+  if (mr <= 0 || ncols <= 0) return RRF_OK;
+  const double e = (double)sizeof(T);
+  const int sr0 = red_splits(mr, ncols, p->num_cus);
+  ReduceArgs<T> ra{};
+  ra.X = X; ra.ldx = ldx; ra.mr = mr; ra.n = ncols;
+  ra.V = V; ra.ldv = ldv; ra.bp = bp;
+  ra.Z = (T*)p->Zpart; ra.split_stride = ncols * bp;
+  ra.rows_per_split = round_up(ceil_div(mr, sr0), kRedChunk);
+  const int sr = (int)ceil_div(mr, ra.rows_per_split);
+  const double fl = 2.0 * mr * ncols * b;
+  RRF_LAUNCH(p, stage == RRF_STAGE_UPDATE ? RRF_STAGE_REDUCE : stage, fl,
+             e * mr * ncols, launch_reduce<T>(ra, sr, p->stream));
+  FormWArgs<T> fa{};
+  fa.Z = (T*)p->Zpart; fa.nsplit = sr; fa.split_stride = ra.split_stride;
+  fa.Tm = Tm; fa.ldt = ldt; fa.W = (T*)p->W; fa.n = ncols; fa.bp = bp;
+  fa.trans = trans;
+  fa.b = b;
+  RRF_LAUNCH(p, stage == RRF_STAGE_UPDATE ? RRF_STAGE_FORMW : stage,
+             (double)ncols * b * b, e * ncols * b * (sr + 1),
+             launch_formw<T>(fa, p->stream));
+  UpdateArgs<T> ua{};
+  ua.src = X; ua.lds = ldx; ua.dst = X; ua.ldd = ldx; ua.mr = mr; ua.n = ncols;
+  ua.V = V; ua.ldv = ldv; ua.bp = bp; ua.W = (T*)p->W; ua.ldw = bp;
+  ua.Om = nullptr; ua.ldo = kOmLd; ua.qp = 0; ua.P = nullptr; ua.ldp = 0;
+  ua.split_stride = 0; ua.s0 = 0; ua.normpart = nullptr;
+  const int su0 = upd_splits(mr, ncols, p->num_cus);
+  ua.cols_per_split = round_up(ceil_div(ncols, su0), kUpdChunk);
+  const int su = (int)ceil_div(ncols, ua.cols_per_split);
+  RRF_LAUNCH(p, stage, fl, 2.0 * e * mr * ncols, launch_update<T>(ua, su, p->stream));
+  return RRF_OK;
+}
+
+template <typename T>
+rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
+                    double tol, int64_t b, uint64_t seed, int64_t* k_out,
+                    bool* warn_kmax) {
+  hipStream_t s = p->stream;
+  const int64_t ldb = p->sz.ldb;
+  T* Bws = (T*)p->Bws;
+  double* V = p->V;
+  double* Tm = p->Tm;
+  double* tau = p->tau;
+  T* Yp = (T*)p->Ypart;
+  T* Om = (T*)p->Om;
+  T* Q = (T*)p->Q;
+  const double e = (double)p->elem;
+  int64_t kcap = std::min(m, n);
+  if (p->k_max > 0) kcap = std::min(kcap, p->k_max);
+  const int mode = p->stop_mode;
+  p->trace_trail.clear();
+  p->trace_sub.clear();
+  p->block_start.clear();
+  p->nblocks = 0;
+
+  // Initial sample Y_0 = A Omega_0 and ||A||_F^2 in one read of A.
+  const int64_t b0 = std::min(b, kcap);
+  const int q0 = b0 > 0 ? pad16(b0) : 0;
+  if (b0 > 0)
+    RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b0,
+               launch_sketch<T>(seed, n, 0, b0, Om, kOmLd, 1, s));
+  UpdateArgs<T> u{};
+  u.src = A; u.lds = lda; u.dst = nullptr; u.ldd = 0; u.mr = m; u.n = n;
+  u.V = nullptr; u.ldv = 0; u.bp = 0; u.W = nullptr; u.ldw = 0;
+  u.Om = Om; u.ldo = kOmLd; u.qp = q0; u.P = Yp; u.ldp = ldb;
+  u.split_stride = ldb * 64; u.s0 = 0; u.normpart = p->normpart;
+  {
+    const int su0 = upd_splits(m, n, p->num_cus);
+    u.cols_per_split = round_up(ceil_div(n, su0), kUpdChunk);
+  }
+  int ysplits = (int)ceil_div(n, u.cols_per_split);
+  RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 2.0 * m * n * b0, e * (m * n + m * b0),
+             launch_update<T>(u, ysplits, s));
+  int nparts = (int)(ceil_div(m, kUpdRows) * ysplits);
+  RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
+             launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
+                             p->trace_sub_d, 0, 0, kcap, mode, tol, 1, s));
+  hipError_t he = read_state(p);
+  if (he != hipSuccess) return hip_fail(he);
+  if (p->st_host->nonfinite) return RRF_ERR_NONFINITE;
+
+  int64_t k = 0;
+  int64_t yoff = 0;
+  int blk = 0;
+  bool stop = p->st_host->stop != 0;
+  while (!stop) {
+    const int64_t bi = std::min(b, kcap - k);
+    const int bp = pad16(bi);
+    const int64_t mp = m - k;
+    p->block_start.push_back(k);
+    PanelShape sh;
+    if (!panel_shape(mp, (int)bi, p->num_cus, p->panel_target, &sh)) return RRF_ERR_SHAPE;
+    PanelArgs<T> pa{};
+    pa.Y = Yp + yoff; pa.ldy = ldb; pa.nsplit = ysplits; pa.split_stride = ldb * 64;
+    pa.m = mp; pa.b = (int)bi;
+    pa.V = V + k + k * ldb; pa.ldv = ldb;
+    pa.Tm = Tm + k * kTLd; pa.ldt = kTLd; pa.tau = tau + k;
+    pa.red = p->red; pa.rowj = p->rowj; pa.bar = p->bar; pa.st = p->st; pa.G = sh.G;
+    RRF_LAUNCH(p, RRF_STAGE_PANEL,
+               2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi,
+               e * 2.0 * mp * bi, launch_panel<T>(pa, sh, s));
+
+    const T* src = blk == 0 ? A : Bws;
+    const int64_t lsrc = blk == 0 ? lda : ldb;
+    // Z = V_i^T B[k:m, :], W = T_i^T Z.
+    const int sr0 = red_splits(mp, n, p->num_cus);
+    ReduceArgs<T> ra{};
+    ra.X = src + k; ra.ldx = lsrc; ra.mr = mp; ra.n = n;
+    ra.V = V + k + k * ldb; ra.ldv = ldb; ra.bp = bp;
+    ra.Z = (T*)p->Zpart; ra.split_stride = n * bp;
+    ra.rows_per_split = round_up(ceil_div(mp, sr0), kRedChunk);
+    const int sr = (int)ceil_div(mp, ra.rows_per_split);
+    RRF_LAUNCH(p, RRF_STAGE_REDUCE, 2.0 * mp * n * bi, e * mp * n,
+               launch_reduce<T>(ra, sr, s));
+    FormWArgs<T> fa{};
+    fa.Z = (T*)p->Zpart; fa.nsplit = sr; fa.split_stride = ra.split_stride;
+    fa.Tm = Tm + k * kTLd; fa.ldt = kTLd; fa.W = (T*)p->W; fa.n = n; fa.bp = bp;
+    fa.trans = 1;
+    fa.b = (int)bi;
+    RRF_LAUNCH(p, RRF_STAGE_FORMW, 1.0 * n * bi * bi, e * n * bi * (sr + 1),
+               launch_formw<T>(fa, s));
+
+    // Next sketch block (speculative: the stop test comes after the update).
+    const int64_t k_next = k + bi;
+    const int64_t b_next = k_next < kcap ? std::min(b, kcap - k_next) : 0;
+    const int q_next = b_next > 0 ? pad16(b_next) : 0;
+    if (b_next > 0)
+      RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
+                 launch_sketch<T>(seed, n, k_next, b_next, Om, kOmLd, 1, s));
+
+    // B[k:m, :] -= V_i W, fused with the next sample and the norms.
+    UpdateArgs<T> ua{};
+    ua.src = src + k; ua.lds = lsrc; ua.dst = Bws + k; ua.ldd = ldb;
+    ua.mr = mp; ua.n = n; ua.V = V + k + k * ldb; ua.ldv = ldb; ua.bp = bp;
+    ua.W = (T*)p->W; ua.ldw = bp; ua.Om = Om; ua.ldo = kOmLd; ua.qp = q_next;
+    ua.P = Yp; ua.ldp = ldb; ua.split_stride = ldb * 64; ua.s0 = bi;
+    ua.normpart = p->normpart;
+    const int su0 = upd_splits(mp, n, p->num_cus);
+    ua.cols_per_split = round_up(ceil_div(n, su0), kUpdChunk);
+    const int su = (int)ceil_div(n, ua.cols_per_split);
+    RRF_LAUNCH(p, RRF_STAGE_UPDATE,
+               2.0 * mp * n * bi + 2.0 * (mp - bi) * n * b_next,
+               2.0 * e * mp * n, launch_update<T>(ua, su, s));
+    nparts = (int)(ceil_div(mp, kUpdRows) * su);
+    RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
+               launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
+                               p->trace_sub_d, blk, k_next, kcap, mode, tol, 0, s));
+    he = read_state(p);
+    if (he != hipSuccess) return hip_fail(he);
+    k = k_next;
+    ++blk;
+    yoff = bi;
+    ysplits = su;
+    if (p->st_host->barrier_err) return RRF_ERR_INTERNAL;
+    if (p->st_host->nonfinite) return RRF_ERR_NONFINITE;
+    stop = p->st_host->stop != 0;
+  }
+  p->nblocks = blk;
+
+  // Explicit Q = H_0 ... H_{k-1} [I_k; 0], backward over the blocks, in
+  // binary64 (float plans round the result once).
+  if (k > 0) {
+    double* Qd = std::is_same<T, double>::value ? (double*)Q : (double*)p->Q64;
+    RRF_LAUNCH(p, RRF_STAGE_ORGQR, 0.0, 8.0 * m * k,
+               launch_fill_identity<double>(Qd, ldb, m, k, s));
+    for (int i = blk - 1; i >= 0; --i) {
+      const int64_t ki = p->block_start[i];
+      const int64_t bi = (i + 1 < blk ? p->block_start[i + 1] : k) - ki;
+      rrf_status rs = apply_wy<double>(p, 0, V + ki + ki * ldb, ldb,
+                                       Tm + ki * kTLd, kTLd, (int)bi, pad16(bi),
+                                       Qd + ki + ki * ldb, ldb, m - ki, k - ki,
+                                       RRF_STAGE_ORGQR);
+      if (rs != RRF_OK) return rs;
+    }
+    if (!std::is_same<T, double>::value)
+      RRF_LAUNCH(p, RRF_STAGE_ORGQR, 0.0, 12.0 * m * k,
+                 (launch_convert<double, float>(Qd, ldb, (float*)Q, ldb, m, k, s)));
+  }
+  he = hipStreamSynchronize(s);
+  if (he != hipSuccess) return hip_fail(he);
+
+  // Trace back to the host.
+  if (blk > 0) {
+    p->trace_trail.resize(blk);
+    p->trace_sub.resize(blk);
+    he = hipMemcpy(p->trace_trail.data(), p->trace_trail_d, blk * sizeof(double),
+                   hipMemcpyDeviceToHost);
+    if (he == hipSuccess)
+      he = hipMemcpy(p->trace_sub.data(), p->trace_sub_d, blk * sizeof(double),
+                     hipMemcpyDeviceToHost);
+    if (he != hipSuccess) return hip_fail(he);
+  }
+  p->E0 = p->st_host->E0;
+  p->sigma2 = p->st_host->sigma2;
+  const double E = mode ? p->st_host->E_sub : p->st_host->E_trail;
+  *warn_kmax = k == kcap && kcap < std::min(m, n) && E > p->sigma2;
+  *k_out = k;
+  return RRF_OK;
+}
+
+bool valid_dtype(int d) { return d == RRF_F32 || d == RRF_F64; }
+
+template <typename T>
+hipError_t to_plan_type(const double* src, int64_t lds, T* dst, int64_t ldd,
+                        int64_t rows, int64_t cols, hipStream_t s) {
+  if (std::is_same<T, double>::value)
+    return launch_copy<double>(src, lds, (double*)dst, ldd, rows, cols, s);
+  return launch_convert<double, float>(src, lds, (float*)dst, ldd, rows, cols, s);
+}
+
+template <typename T>
+hipError_t from_plan_type(const T* src, int64_t lds, double* dst, int64_t ldd,
+                          int64_t rows, int64_t cols, hipStream_t s) {
+  if (std::is_same<T, double>::value)
+    return launch_copy<double>((const double*)src, lds, dst, ldd, rows, cols, s);
+  return launch_convert<float, double>((const float*)src, lds, dst, ldd, rows, cols, s);
+}
+
+template <typename T>
+rrf_status panel_stage(rrf_plan* p, const T* Y, int64_t m, int64_t b,
+                       int64_t ldy, T* Vout, int64_t ldv, T* Tout, int64_t ldt,
+                       T* tauout) {
+  PanelShape sh;
+  if (!panel_shape(m, (int)b, p->num_cus, p->panel_target, &sh)) return RRF_ERR_SHAPE;
+  hipStream_t s = p->stream;
+  PanelArgs<T> pa{};
+  pa.Y = Y; pa.ldy = ldy; pa.nsplit = 1; pa.split_stride = 0;
+  pa.m = m; pa.b = (int)b;
+  pa.V = p->V; pa.ldv = p->sz.ldb;
+  pa.Tm = p->Tm; pa.ldt = kTLd; pa.tau = p->tau;
+  pa.red = p->red; pa.rowj = p->rowj; pa.bar = p->bar; pa.st = p->st; pa.G = sh.G;
+  hipError_t e = launch_panel<T>(pa, sh, s);
+  if (e == hipSuccess) e = to_plan_type<T>(p->V, p->sz.ldb, Vout, ldv, m, b, s);
+  if (e == hipSuccess) e = to_plan_type<T>(p->Tm, kTLd, Tout, ldt, b, b, s);
+  if (e == hipSuccess) e = to_plan_type<T>(p->tau, 1, tauout, 1, b, 1, s);
+  return e == hipSuccess ? RRF_OK : hip_fail(e);
+}
+
+template <typename T>
+rrf_status larfb_stage(rrf_plan* p, int trans, const T* V, int64_t ldv,
+                       const T* Tm, int64_t ldt, int64_t b, T* X, int64_t m,
+                       int64_t n, int64_t ldx) {
+  hipStream_t s = p->stream;
+  const int bp = pad16(b);
+  const int64_t ldb = p->sz.ldb;
+  double* Vw = p->V;
+  double* Tw = p->Tm;
+  // Zero-padded binary64 copies of V (m x bp) and T (bp x bp).
+  hipError_t e = hipMemsetAsync(Vw, 0, (size_t)ldb * bp * sizeof(double), s);
+  if (e == hipSuccess) e = hipMemsetAsync(Tw, 0, (size_t)kTLd * bp * sizeof(double), s);
+  if (e == hipSuccess) e = from_plan_type<T>(V, ldv, Vw, ldb, m, b, s);
+  if (e == hipSuccess) e = from_plan_type<T>(Tm, ldt, Tw, kTLd, b, b, s);
+  if (e != hipSuccess) return hip_fail(e);
+  stats_reset(p);
+  return apply_wy<T>(p, trans, Vw, ldb, Tw, kTLd, (int)b, bp, X, ldx, m, n,
+                     RRF_STAGE_UPDATE);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rrf_status_string(rrf_status s) {
+  switch (s) {
+    case RRF_OK: return "RRF_OK";
+    case RRF_WARN_KMAX: return "RRF_WARN_KMAX: rank cap reached before the tolerance";
+    case RRF_ERR_INVALID_ARG: return "RRF_ERR_INVALID_ARG: invalid argument";
+    case RRF_ERR_SHAPE: return "RRF_ERR_SHAPE: size exceeds the plan or the panel capacity";
+    case RRF_ERR_NONFINITE: return "RRF_ERR_NONFINITE: non-finite input or norm";
+    case RRF_ERR_NOMEM: return "RRF_ERR_NOMEM: allocation failed";
+    case RRF_ERR_HIP: return "RRF_ERR_HIP: HIP runtime error";
+    case RRF_ERR_INTERNAL: return "RRF_ERR_INTERNAL: device-side wait gave up";
+  }
+  return "RRF: unknown status";
+}
+
+rrf_status rrf_workspace_size(rrf_dtype dtype, int64_t m_max, int64_t n_max,
+                              int64_t block_b_max, int64_t k_max,
+                              size_t* bytes) {
+  if (!bytes || !valid_dtype(dtype) || m_max < 1 || n_max < 1 ||
+      block_b_max < 1 || block_b_max > kMaxBlock || k_max < 0)
+    return RRF_ERR_INVALID_ARG;
+  *bytes = compute_sizes(dtype, m_max, n_max, block_b_max, k_max).total();
+  return RRF_OK;
+}
+
+rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
+                           int64_t n_max, int64_t block_b_max, int64_t k_max,
+                           void* hip_stream) {
+  if (!plan || !valid_dtype(dtype) || m_max < 1 || n_max < 1 ||
+      block_b_max < 1 || block_b_max > kMaxBlock || k_max < 0)
+    return RRF_ERR_INVALID_ARG;
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return RRF_ERR_HIP;
+  rrf_plan* p = new (std::nothrow) rrf_plan();
+  if (!p) return RRF_ERR_NOMEM;
+  p->dtype = dtype;
+  p->elem = dtype == RRF_F32 ? 4 : 8;
+  p->m_max = m_max;
+  p->n_max = n_max;
+  p->b_max = block_b_max;
+  p->k_max = k_max;
+  p->stream = (hipStream_t)hip_stream;
+  p->stop_mode = RRF_STOP_TRAILING;
+  p->timing = 0;
+  p->panel_target = 64;
+  if (const char* pt = std::getenv("RRF_PANEL_WGS")) {
+    const int v = std::atoi(pt);
+    if (v >= 1 && v <= kMaxPanelWGs) p->panel_target = v;
+  }
+  if (hipGetDevice(&p->device) != hipSuccess ||
+      hipDeviceGetAttribute(&p->num_cus, hipDeviceAttributeMultiprocessorCount,
+                            p->device) != hipSuccess) {
+    free_plan(p);
+    return RRF_ERR_HIP;
+  }
+  // The first panel has m_max rows; it must fit the register-resident panel.
+  PanelShape sh;
+  if (!panel_shape(std::max(m_max, block_b_max), (int)block_b_max, p->num_cus,
+                   p->panel_target, &sh)) {
+    free_plan(p);
+    return RRF_ERR_SHAPE;
+  }
+  p->sz = compute_sizes(dtype, m_max, n_max, block_b_max, k_max);
+  int counter = 0;
+  hipError_t e = hipSuccess;
+  void* tmp = nullptr;
+#define RRF_ALLOC(field, bytes)                                     \
+  do {                                                              \
+    if (e == hipSuccess) {                                          \
+      e = dev_alloc(p, &tmp, (bytes), &counter);                    \
+      p->field = reinterpret_cast<decltype(p->field)>(tmp);         \
+    }                                                               \
+  } while (0)
+  RRF_ALLOC(Bws, p->sz.Bws);
+  RRF_ALLOC(V, p->sz.V);
+  RRF_ALLOC(Tm, p->sz.Tm);
+  RRF_ALLOC(tau, p->sz.tau);
+  RRF_ALLOC(Ypart, p->sz.Ypart);
+  RRF_ALLOC(Om, p->sz.Om);
+  RRF_ALLOC(Zpart, p->sz.Zpart);
+  RRF_ALLOC(W, p->sz.W);
+  RRF_ALLOC(Q, p->sz.Q);
+  if (p->sz.Q64) RRF_ALLOC(Q64, p->sz.Q64);
+  RRF_ALLOC(normpart, p->sz.normpart);
+  RRF_ALLOC(red, p->sz.red);
+  RRF_ALLOC(rowj, p->sz.rowj);
+  RRF_ALLOC(bar, p->sz.bar);
+  RRF_ALLOC(st, p->sz.st);
+  RRF_ALLOC(trace_trail_d, p->sz.trace / 2);
+  RRF_ALLOC(trace_sub_d, p->sz.trace / 2);
+#undef RRF_ALLOC
+  if (e == hipSuccess) {
+    ++counter;
+    const char* f = std::getenv("RRF_FAULT_ALLOC");
+    if (f && std::atoi(f) == counter) e = hipErrorOutOfMemory;
+    else e = hipHostMalloc((void**)&p->st_host, sizeof(DevState), 0);
+  }
+  if (e == hipSuccess) e = hipMemsetAsync(p->bar, 0, p->sz.bar, p->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(p->st, 0, p->sz.st, p->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(p->Om, 0, p->sz.Om, p->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(p->V, 0, p->sz.V, p->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(p->stream);
+  if (e != hipSuccess) {
+    free_plan(p);
+    return hip_fail(e);
+  }
+  stats_reset(p);
+  p->last_m = p->last_n = p->last_k = p->nblocks = 0;
+  p->last_b = 0;
+  p->E0 = p->sigma2 = 0.0;
+  *plan = p;
+  return RRF_OK;
+}
+
+rrf_status rrf_destroy(rrf_plan_t plan) {
+  if (!plan) return RRF_OK;
+  (void)hipStreamSynchronize(plan->stream);
+  free_plan(plan);
+  return RRF_OK;
+}
+
+rrf_status rrf_set_stop_mode(rrf_plan_t plan, rrf_stop_mode mode) {
+  if (!plan || (mode != RRF_STOP_TRAILING && mode != RRF_STOP_SUBTRACT))
+    return RRF_ERR_INVALID_ARG;
+  plan->stop_mode = mode;
+  return RRF_OK;
+}
+
+rrf_status rrf_set_timing(rrf_plan_t plan, int enable) {
+  if (!plan) return RRF_ERR_INVALID_ARG;
+  plan->timing = enable ? 1 : 0;
+  return RRF_OK;
+}
+
+rrf_status rrf_run(rrf_plan_t plan, const void* A, int64_t m, int64_t n,
+                   int64_t lda, double tol, int64_t block_b, uint64_t seed,
+                   void** Q, int64_t* ldq, int64_t* k, void** B, int64_t* ldb) {
+  if (!plan || !A || !Q || !ldq || !k || !B || !ldb) return RRF_ERR_INVALID_ARG;
+  if (m < 0 || n < 0 || lda < std::max<int64_t>(1, m)) return RRF_ERR_INVALID_ARG;
+  if (!std::isfinite(tol) || tol < 0.0) return RRF_ERR_INVALID_ARG;
+  if (block_b < 1 || block_b > plan->b_max) return RRF_ERR_INVALID_ARG;
+  if (m > plan->m_max || n > plan->n_max) return RRF_ERR_SHAPE;
+  stats_reset(plan);
+  plan->last_m = m;
+  plan->last_n = n;
+  plan->last_b = block_b;
+  plan->last_k = 0;
+  plan->nblocks = 0;
+  int64_t kk = 0;
+  bool warn = false;
+  rrf_status st = RRF_OK;
+  if (m > 0 && n > 0) {
+    if (plan->dtype == RRF_F64)
+      st = run_impl<double>(plan, (const double*)A, m, n, lda, tol, block_b,
+                            seed, &kk, &warn);
+    else
+      st = run_impl<float>(plan, (const float*)A, m, n, lda, tol, block_b, seed,
+                           &kk, &warn);
+    if (st != RRF_OK) {
+      (void)hipStreamSynchronize(plan->stream);
+      if (plan->st_host && plan->st_host->barrier_err) {
+        (void)launch_zero_u32(plan->bar, 2, plan->stream);
+        (void)hipStreamSynchronize(plan->stream);
+      }
+      plan->nblocks = 0;
+      *k = 0;
+      return st;
+    }
+    stats_collect(plan);
+  }
+  plan->last_k = kk;
+  *Q = plan->Q;
+  *ldq = plan->sz.ldb;
+  *B = plan->Bws;
+  *ldb = plan->sz.ldb;
+  *k = kk;
+  return warn ? RRF_WARN_KMAX : RRF_OK;
+}
+
+rrf_status rrf_get_trace(rrf_plan_t plan, int64_t cap, int64_t* nblocks,
+                         double* E_trail, double* E_sub, double* E0,
+                         double* sigma2) {
+  if (!plan || !nblocks || cap < 0 || (cap > 0 && (!E_trail || !E_sub)))
+    return RRF_ERR_INVALID_ARG;
+  *nblocks = plan->nblocks;
+  const int64_t nw = std::min<int64_t>(cap, plan->nblocks);
+  for (int64_t i = 0; i < nw; ++i) {
+    E_trail[i] = plan->trace_trail[i];
+    E_sub[i] = plan->trace_sub[i];
+  }
+  if (E0) *E0 = plan->E0;
+  if (sigma2) *sigma2 = plan->sigma2;
+  return RRF_OK;
+}
+
+rrf_status rrf_get_stage_stats(rrf_plan_t plan, double* ms, int64_t* launches,
+                               double* flops, double* bytes) {
+  if (!plan) return RRF_ERR_INVALID_ARG;
+  for (int i = 0; i < RRF_NUM_STAGES; ++i) {
+    if (ms) ms[i] = plan->ms[i];
+    if (launches) launches[i] = plan->launches[i];
+    if (flops) flops[i] = plan->flops[i];
+    if (bytes) bytes[i] = plan->bytes[i];
+  }
+  return RRF_OK;
+}
+
+rrf_status rrf_get_reflectors(rrf_plan_t plan, const void** V, int64_t* ldv,
+                              const void** T, int64_t* ldt, const void** tau) {
+  if (!plan || !V || !ldv || !T || !ldt || !tau) return RRF_ERR_INVALID_ARG;
+  // Zero V above each block (the kernels never touch those rows).
+  if (plan->last_k > 0) {
+    const int64_t ldb = plan->sz.ldb;
+    for (size_t i = 0; i < plan->block_start.size(); ++i) {
+      const int64_t ki = plan->block_start[i];
+      const int64_t bi = (i + 1 < plan->block_start.size() ? plan->block_start[i + 1]
+                                                            : plan->last_k) - ki;
+      if (ki == 0) continue;
+      for (int64_t c = 0; c < bi; ++c) {
+        hipError_t e = hipMemsetAsync(plan->V + (ki + c) * ldb, 0,
+                                      ki * sizeof(double), plan->stream);
+        if (e != hipSuccess) return hip_fail(e);
+      }
+    }
+    hipError_t e = hipStreamSynchronize(plan->stream);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  *V = plan->V;
+  *ldv = plan->sz.ldb;
+  *T = plan->Tm;
+  *ldt = kTLd;
+  *tau = plan->tau;
+  return RRF_OK;
+}
+
+rrf_status rrf_sketch(rrf_dtype dtype, uint64_t seed, int64_t n, int64_t col0,
+                      int64_t ncols, void* out, int64_t ldo, void* hip_stream) {
+  if (!valid_dtype(dtype) || !out || n < 0 || col0 < 0 || ncols < 0 ||
+      ldo < std::max<int64_t>(1, n))
+    return RRF_ERR_INVALID_ARG;
+  if (n == 0 || ncols == 0) return RRF_OK;
+  hipError_t e;
+  if (dtype == RRF_F64)
+    e = launch_sketch<double>(seed, n, col0, ncols, (double*)out, 1, ldo,
+                              (hipStream_t)hip_stream);
+  else
+    e = launch_sketch<float>(seed, n, col0, ncols, (float*)out, 1, ldo,
+                             (hipStream_t)hip_stream);
+  return e == hipSuccess ? RRF_OK : hip_fail(e);
+}
+
+
+rrf_status rrf_panel_qr(rrf_plan_t plan, const void* Y, int64_t m, int64_t b,
+                        int64_t ldy, void* V, int64_t ldv, void* T,
+                        int64_t ldt, void* tau) {
+  if (!plan || !Y || !V || !T || !tau) return RRF_ERR_INVALID_ARG;
+  if (b < 1 || b > plan->b_max || m < b || ldy < m || ldv < m || ldt < b)
+    return RRF_ERR_INVALID_ARG;
+  if (m > plan->m_max) return RRF_ERR_SHAPE;
+  if (plan->dtype == RRF_F64)
+    return panel_stage<double>(plan, (const double*)Y, m, b, ldy, (double*)V,
+                               ldv, (double*)T, ldt, (double*)tau);
+  return panel_stage<float>(plan, (const float*)Y, m, b, ldy, (float*)V, ldv,
+                            (float*)T, ldt, (float*)tau);
+}
+
+rrf_status rrf_apply_block_reflector(rrf_plan_t plan, int trans,
+                                     const void* V, int64_t ldv,
+                                     const void* T, int64_t ldt, int64_t b,
+                                     void* X, int64_t m, int64_t n,
+                                     int64_t ldx) {
+  if (!plan || !V || !T || !X) return RRF_ERR_INVALID_ARG;
+  if (b < 1 || b > plan->b_max || m < 0 || n < 0 || ldv < std::max<int64_t>(1, m) ||
+      ldt < b || ldx < std::max<int64_t>(1, m))
+    return RRF_ERR_INVALID_ARG;
+  if (m > plan->m_max || n > plan->n_max) return RRF_ERR_SHAPE;
+  if (m == 0 || n == 0) return RRF_OK;
+  if (plan->dtype == RRF_F64)
+    return larfb_stage<double>(plan, trans, (const double*)V, ldv,
+                               (const double*)T, ldt, b, (double*)X, m, n, ldx);
+  return larfb_stage<float>(plan, trans, (const float*)V, ldv, (const float*)T,
+                            ldt, b, (float*)X, m, n, ldx);
+}
+
+rrf_status rrf_copy_matrix(rrf_dtype dtype, const void* src, int64_t lds,
+                           void* dst, int64_t ldd, int64_t rows, int64_t cols,
+                           void* hip_stream) {
+  if (!valid_dtype(dtype) || !src || !dst || rows < 0 || cols < 0 ||
+      lds < std::max<int64_t>(1, rows) || ldd < std::max<int64_t>(1, rows))
+    return RRF_ERR_INVALID_ARG;
+  hipError_t e;
+  if (dtype == RRF_F64)
+    e = launch_copy<double>((const double*)src, lds, (double*)dst, ldd, rows,
+                            cols, (hipStream_t)hip_stream);
+  else
+    e = launch_copy<float>((const float*)src, lds, (float*)dst, ldd, rows, cols,
+                           (hipStream_t)hip_stream);
+  return e == hipSuccess ? RRF_OK : hip_fail(e);
+}
+
+}  // extern "C"

@@ -1,0 +1,124 @@
+// Internal declarations shared by the HIP sources of librrf.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/rrf.h"
+
+namespace rrf {
+
+// Tiling constants (see each kernel for its use).
+constexpr int kMaxBlock = 64;      // largest block size b (MFMA tiles of 16)
+constexpr int kUpdRows = 64;       // rows per update workgroup (4 waves x 16)
+constexpr int kUpdChunk = 32;      // columns per staged chunk in the update
+constexpr int kRedCols = 64;       // columns per reduce workgroup (4 waves x 16)
+constexpr int kRedChunk = 64;      // rows per staged V chunk in the reduce
+constexpr int kPanelThreads = 256;
+constexpr int kMaxPanelWGs = 1024;
+
+inline int pad16(int64_t b) { return b <= 16 ? 16 : (b <= 32 ? 32 : 64); }
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+// Device-side run state (one per plan).
+struct DevState {
+  double E0;        // ||A||_F^2
+  double sigma2;    // (tol ||A||_F)^2
+  double E_trail;   // ||B[k:m, :]||_F^2 after the last block
+  double E_sub;     // running difference (paper's rule), clamped at 0
+  int stop;         // 1: stop after this block
+  int nonfinite;    // 1: a norm was NaN / Inf
+  int barrier_err;  // 1: a panel grid barrier gave up waiting
+  int pad;
+};
+
+// Launch descriptors -------------------------------------------------------
+
+template <typename T>
+struct UpdateArgs {
+  const T* src; int64_t lds;   // region rows start at the pointer
+  T* dst; int64_t ldd;         // nullptr: do not store
+  int64_t mr, n;               // region rows / columns
+  const double* V; int64_t ldv;  // mr x bp, zero padded (binary64 for both
+  int bp;                        // dtypes; 0: no reflector update)
+  const T* W; int ldw;         // W[c * ldw + p], n x bp
+  const T* Om; int ldo;        // Omega[c * ldo + q], n x qp
+  int qp;                      // 0: no sample
+  T* P; int64_t ldp; int64_t split_stride;  // P_s[r + q * ldp], per column split
+  int64_t s0;                  // rows < s0: block-row norm; >= s0: trailing norm
+  double* normpart;            // 2 doubles per workgroup, or nullptr
+  int64_t cols_per_split;
+};
+
+template <typename T>
+struct ReduceArgs {
+  const T* X; int64_t ldx;     // mr x n region
+  int64_t mr, n;
+  const double* V; int64_t ldv; int bp;
+  T* Z; int64_t split_stride;  // Z_s[c * bp + p]
+  int64_t rows_per_split;
+};
+
+template <typename T>
+struct FormWArgs {
+  const T* Z; int nsplit; int64_t split_stride;
+  const double* Tm; int64_t ldt;  // bp x bp upper triangular (binary64)
+  T* W;                        // W[c * bp + p]
+  int64_t n; int bp;
+  int b;                       // block width: T rows / columns >= b are ignored
+  int trans;                   // 1: W = T^T Z,  0: W = T Z
+};
+
+template <typename T>
+struct PanelArgs {
+  const T* Y; int64_t ldy; int nsplit; int64_t split_stride;
+  int64_t m; int b;            // panel rows, columns (b <= BP)
+  double* V; int64_t ldv;      // m x BP output (binary64 for both dtypes)
+  double* Tm; int64_t ldt;     // BP x BP output
+  double* tau;                 // b outputs
+  double* red;                 // 2 x G x BP
+  double* rowj;                // 2 x BP
+  unsigned* bar;               // {count, generation}
+  DevState* st;
+  int G;
+};
+
+// Launchers (return hipError_t of the launch) ------------------------------
+
+template <typename T>
+hipError_t launch_sketch(uint64_t seed, int64_t n, int64_t col0, int64_t ncols,
+                         T* out, int64_t row_stride, int64_t col_stride,
+                         hipStream_t s);
+template <typename T>
+hipError_t launch_update(const UpdateArgs<T>& a, int nsplit, hipStream_t s);
+template <typename T>
+hipError_t launch_reduce(const ReduceArgs<T>& a, int nsplit, hipStream_t s);
+template <typename T>
+hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s);
+
+// Panel: picks rows-per-thread and grid size; returns hipErrorInvalidValue
+// if the panel does not fit the register-resident capacity.
+struct PanelShape { int bp, rpt, G; };
+bool panel_shape(int64_t m, int b, int num_cus, int target_wgs, PanelShape* out);
+template <typename T>
+hipError_t launch_panel(const PanelArgs<T>& a, const PanelShape& sh,
+                        hipStream_t s);
+
+hipError_t launch_finalize(const double* normpart, int nparts, DevState* st,
+                           double* trace_trail, double* trace_sub, int block,
+                           int64_t k_after, int64_t k_cap, int mode,
+                           double tol, int init, hipStream_t s);
+template <typename T>
+hipError_t launch_fill_identity(T* Q, int64_t ldq, int64_t m, int64_t k,
+                                hipStream_t s);
+template <typename T>
+hipError_t launch_copy(const T* src, int64_t lds, T* dst, int64_t ldd,
+                       int64_t rows, int64_t cols, hipStream_t s);
+template <typename Ts, typename Td>
+hipError_t launch_convert(const Ts* src, int64_t lds, Td* dst, int64_t ldd,
+                          int64_t rows, int64_t cols, hipStream_t s);
+hipError_t launch_zero_u32(unsigned* p, int count, hipStream_t s);
+
+}  // namespace rrf

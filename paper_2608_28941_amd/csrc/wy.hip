@@ -1,0 +1,314 @@
+// Blocked WY reflector application (Alg. 2, update step) and the fused sample
+// of the next sketch block.
+//
+// The block update B <- Q_i^T B = B - V_i T_i^T (V_i^T B) (Theorem 3.1:
+// A~ = Q_1^T A; compact WY form Eq. (4)) runs as three kernels:
+//   reduce  Z_s = V_i^T B[rows of split s, :]      (b x n per split)
+//   formW   W   = T_i^T sum_s Z_s                  (b x n)
+//   update  B  -= V_i W, and in the same pass over B
+//           P   = B_new Omega_{i+1}  (next sample, Alg. 2 sketch/qr steps)
+//           ||B_new[rows < s0]||^2, ||B_new[rows >= s0]||^2  (Alg. 2 E step,
+//           fused as the paper's outlook suggests)
+// With trans = 0 the same kernels apply Q_i = I - V_i T_i V_i^T (explicit Q).
+//
+// Both GEMM-shaped kernels run on MFMA 16x16x4 (f64 or f32).  V and T are
+// kept in binary64 for both dtypes; the f32 kernels round V on load.  They are
+// written in the transposed frame so that the 16 lanes of an MFMA column index
+// consecutive rows of the column-major B: each wavefront load or store then
+// touches 16 contiguous rows (128 B of f64) of 4 columns.
+//   update: a wavefront owns 16 rows; its slice of V (16 x b) stays in
+//           registers for the whole sweep over the columns; W and Omega
+//           chunks are staged in LDS and shared by the 4 wavefronts.
+//   reduce: a wavefront owns 16 columns and all b reflectors; V rows are
+//           staged in LDS and shared; B is read straight into registers.
+
+#include "mfma.h"
+#include "rrf_internal.h"
+
+namespace rrf {
+namespace {
+
+// ---------------------------------------------------------------------------
+// reduce: Z_s[c * BP + p] = sum_{r in split s} V[r, p] X[r, c]
+// grid (ceil(n / 64), nsplit), 256 threads.
+// ---------------------------------------------------------------------------
+template <typename T, int BP>
+__global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs<T> a) {
+  typedef typename Mfma<T>::acc_t acc_t;
+  constexpr int NPT = BP / 16;
+  constexpr int LDV = kRedChunk + 1;
+  __shared__ T vl[BP * LDV];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m16 = lane & 15, g = lane >> 4;
+  const int64_t cb = (int64_t)blockIdx.x * kRedCols + 16 * wave;
+  const int64_t col = cb + m16;
+  const bool colok = col < a.n;
+  const int64_t r_begin = (int64_t)blockIdx.y * a.rows_per_split;
+  const int64_t r_end = min(a.mr, r_begin + a.rows_per_split);
+  const T* Xc = a.X + (colok ? col : 0) * a.ldx;
+
+  acc_t acc[NPT];
+#pragma unroll
+  for (int pt = 0; pt < NPT; ++pt) acc[pt] = Mfma<T>::zero();
+
+  for (int64_t R = r_begin; R < r_end; R += kRedChunk) {
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < BP * kRedChunk; idx += 256) {
+      const int rr = idx % kRedChunk, p = idx / kRedChunk;
+      const int64_t r = R + rr;
+      vl[p * LDV + rr] = (r < r_end) ? (T)a.V[r + p * a.ldv] : T(0);
+    }
+    __syncthreads();
+    const int64_t rows_here = min((int64_t)kRedChunk, r_end - R);
+    for (int s16 = 0; s16 < rows_here; s16 += 16) {
+      T xa[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int64_t r = R + s16 + 4 * s + g;
+        xa[s] = (colok && r < r_end) ? Xc[r] : T(0);
+      }
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+#pragma unroll
+        for (int pt = 0; pt < NPT; ++pt) {
+          const T bv = vl[(pt * 16 + m16) * LDV + s16 + 4 * s + g];
+          acc[pt] = Mfma<T>::op(xa[s], bv, acc[pt]);
+        }
+      }
+    }
+  }
+  // Lane holds Z^T[c = cb + drow(g, i)][p = pt * 16 + m16].
+  T* Z = a.Z + (int64_t)blockIdx.y * a.split_stride;
+#pragma unroll
+  for (int pt = 0; pt < NPT; ++pt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t c = cb + Mfma<T>::drow(g, i);
+      if (c < a.n) Z[c * BP + pt * 16 + m16] = acc[pt][i];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// formW: W[c * BP + p] = (T^T z_c)_p (trans) or (T z_c)_p, z_c = sum_s Z_s[c]
+// Only the leading b x b block of T is used (the padding columns of a stored
+// block may already hold the next block's T), so W rows >= b are zero.
+// ---------------------------------------------------------------------------
+template <typename T, int BP>
+__global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
+  constexpr int CPB = 256 / BP;
+  __shared__ double Tl[BP][BP + 1];
+  __shared__ double zs[CPB][BP + 1];
+  for (int idx = threadIdx.x; idx < BP * BP; idx += 256) {
+    const int i = idx % BP, j = idx / BP;
+    Tl[i][j] = (i <= j && j < a.b) ? a.Tm[i + j * a.ldt] : 0.0;
+  }
+  const int p = threadIdx.x % BP, cl = threadIdx.x / BP;
+  for (int64_t c0 = (int64_t)blockIdx.x * CPB; c0 < a.n;
+       c0 += (int64_t)gridDim.x * CPB) {
+    __syncthreads();
+    const int64_t c = c0 + cl;
+    double z = 0.0;
+    if (c < a.n)
+      for (int s = 0; s < a.nsplit; ++s)
+        z += (double)a.Z[s * a.split_stride + c * BP + p];
+    zs[cl][p] = z;
+    __syncthreads();
+    double w = 0.0;
+    if (a.trans) {
+      for (int l = 0; l <= p; ++l) w += Tl[l][p] * zs[cl][l];
+    } else {
+      for (int l = p; l < BP; ++l) w += Tl[p][l] * zs[cl][l];
+    }
+    if (c < a.n) a.W[c * BP + p] = (T)w;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// update: X <- X - V W (BP > 0), optional store, norms, and P = X_new Omega.
+// grid (ceil(mr / 64), nsplit), 256 threads; wavefront w owns 16 rows.
+// ---------------------------------------------------------------------------
+template <typename T, int BP, int QP>
+__global__ __launch_bounds__(256) void update_kernel(UpdateArgs<T> a) {
+  typedef typename Mfma<T>::acc_t acc_t;
+  constexpr int NP4 = BP / 4;        // K-steps of the rank-b update
+  constexpr int NQT = QP / 16;       // 16-wide tiles of the sample
+  constexpr int LDW = BP + 1;        // odd: conflict-free column reads
+  constexpr int LDO = QP + 1;
+  __shared__ T wl[kUpdChunk * (BP > 0 ? LDW : 1)];
+  __shared__ T ol[kUpdChunk * (QP > 0 ? LDO : 1)];
+  __shared__ double nred[2][4];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m16 = lane & 15, g = lane >> 4;
+  const int64_t r = (int64_t)blockIdx.x * kUpdRows + 16 * wave + m16;
+  const bool rowok = r < a.mr;
+  const int64_t rr = rowok ? r : 0;
+  const int64_t cs = (int64_t)blockIdx.y * a.cols_per_split;
+  const int64_t ce = min(a.n, cs + a.cols_per_split);
+
+  // This wavefront's slice of -V^T as MFMA B operands: B[g][m] = -V[r][4 p4 + g].
+  T vreg[NP4 > 0 ? NP4 : 1];
+#pragma unroll
+  for (int p4 = 0; p4 < NP4; ++p4)
+    vreg[p4] = rowok ? -(T)a.V[rr + (4 * p4 + g) * a.ldv] : T(0);
+
+  acc_t pacc[NQT > 0 ? NQT : 1];
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) pacc[qt] = Mfma<T>::zero();
+  double nb = 0.0, nt = 0.0;
+  const bool in_block = r < a.s0;
+
+  for (int64_t c0 = cs; c0 < ce; c0 += kUpdChunk) {
+    __syncthreads();
+    if (BP > 0) {
+      for (int idx = threadIdx.x; idx < kUpdChunk * BP; idx += 256) {
+        const int p = idx % BP, cc = idx / BP;
+        const int64_t c = c0 + cc;
+        wl[cc * LDW + p] = (c < ce) ? a.W[c * a.ldw + p] : T(0);
+      }
+    }
+    if (QP > 0) {
+      for (int idx = threadIdx.x; idx < kUpdChunk * QP; idx += 256) {
+        const int q = idx % QP, cc = idx / QP;
+        const int64_t c = c0 + cc;
+        ol[cc * LDO + q] = (c < ce) ? a.Om[c * a.ldo + q] : T(0);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ct = 0; ct < kUpdChunk / 16; ++ct) {
+      // D[M = column drow(g, i)][N = row m16] of this 16 x 16 tile.
+      acc_t acc;
+      bool cok[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t c = c0 + ct * 16 + Mfma<T>::drow(g, i);
+        cok[i] = c < ce;
+        acc[i] = (rowok && cok[i]) ? a.src[rr + c * a.lds] : T(0);
+      }
+#pragma unroll
+      for (int p4 = 0; p4 < NP4; ++p4) {
+        const T wa = wl[(ct * 16 + m16) * LDW + 4 * p4 + g];
+        acc = Mfma<T>::op(wa, vreg[p4], acc);
+      }
+      if (a.dst) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t c = c0 + ct * 16 + Mfma<T>::drow(g, i);
+          if (rowok && cok[i]) a.dst[rr + c * a.ldd] = acc[i];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const double v = (rowok && cok[i]) ? (double)acc[i] : 0.0;
+        if (in_block) nb += v * v; else nt += v * v;
+      }
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+#pragma unroll
+        for (int qt = 0; qt < NQT; ++qt) {
+          const T oa = ol[(ct * 16 + Mfma<T>::drow(g, s)) * LDO + qt * 16 + m16];
+          pacc[qt] = Mfma<T>::op(oa, acc[s], pacc[qt]);
+        }
+      }
+    }
+  }
+
+  if (QP > 0 && rowok) {
+    T* P = a.P + (int64_t)blockIdx.y * a.split_stride;
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        P[r + (qt * 16 + Mfma<T>::drow(g, i)) * a.ldp] = pacc[qt][i];
+  }
+  if (a.normpart) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      nb += __shfl_xor(nb, off);
+      nt += __shfl_xor(nt, off);
+    }
+    if (lane == 0) {
+      nred[0][wave] = nb;
+      nred[1][wave] = nt;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const int64_t wg = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+      a.normpart[2 * wg + 0] = ((nred[0][0] + nred[0][1]) + nred[0][2]) + nred[0][3];
+      a.normpart[2 * wg + 1] = ((nred[1][0] + nred[1][1]) + nred[1][2]) + nred[1][3];
+    }
+  }
+}
+
+template <typename T, int BP, int QP>
+hipError_t upd_go(const UpdateArgs<T>& a, dim3 grid, hipStream_t s) {
+  hipLaunchKernelGGL((update_kernel<T, BP, QP>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename T, int BP>
+hipError_t upd_q(const UpdateArgs<T>& a, dim3 grid, hipStream_t s) {
+  switch (a.qp) {
+    case 0: return upd_go<T, BP, 0>(a, grid, s);
+    case 16: return upd_go<T, BP, 16>(a, grid, s);
+    case 32: return upd_go<T, BP, 32>(a, grid, s);
+    case 64: return upd_go<T, BP, 64>(a, grid, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+template <typename T>
+hipError_t launch_update(const UpdateArgs<T>& a, int nsplit, hipStream_t s) {
+  if (a.mr <= 0 || a.n <= 0) return hipSuccess;
+  dim3 grid((unsigned)ceil_div(a.mr, kUpdRows), (unsigned)nsplit);
+  switch (a.bp) {
+    case 0: return upd_q<T, 0>(a, grid, s);
+    case 16: return upd_q<T, 16>(a, grid, s);
+    case 32: return upd_q<T, 32>(a, grid, s);
+    case 64: return upd_q<T, 64>(a, grid, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T>
+hipError_t launch_reduce(const ReduceArgs<T>& a, int nsplit, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  dim3 grid((unsigned)ceil_div(a.n, kRedCols), (unsigned)nsplit);
+  switch (a.bp) {
+    case 16: hipLaunchKernelGGL((reduce_kernel<T, 16>), grid, dim3(256), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((reduce_kernel<T, 32>), grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((reduce_kernel<T, 64>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  const int cpb = 256 / a.bp;
+  int64_t blocks = ceil_div(a.n, cpb);
+  if (blocks > 2048) blocks = 2048;
+  dim3 grid((unsigned)blocks);
+  switch (a.bp) {
+    case 16: hipLaunchKernelGGL((formw_kernel<T, 16>), grid, dim3(256), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((formw_kernel<T, 32>), grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((formw_kernel<T, 64>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template hipError_t launch_update<float>(const UpdateArgs<float>&, int, hipStream_t);
+template hipError_t launch_update<double>(const UpdateArgs<double>&, int, hipStream_t);
+template hipError_t launch_reduce<float>(const ReduceArgs<float>&, int, hipStream_t);
+template hipError_t launch_reduce<double>(const ReduceArgs<double>&, int, hipStream_t);
+template hipError_t launch_formw<float>(const FormWArgs<float>&, hipStream_t);
+template hipError_t launch_formw<double>(const FormWArgs<double>&, hipStream_t);
+
+}  // namespace rrf

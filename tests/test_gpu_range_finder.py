@@ -1,0 +1,219 @@
+"""End-to-end parity of rrf_run against the oracle.
+
+Bar (per workload): the same k; ||Q^T Q - I||_F <= 1e-12 (f64) / 1e-5 (f32);
+||A - Q B||_F / ||A||_F <= 1.05x the oracle's (100 u where both sit at
+roundoff); projector distance <= 1e-8 (f64) / 1e-3 (f32) on spectral-gap
+inputs.  Small and scaled workloads run the oracle live; the five full-size
+workloads compare with the oracle's stored k and residual
+(tests/golden/oracle_configs.json, written by tests/golden/make_golden.py)
+plus the properties that hold at any size.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from tests.gpu_util import (ORTH_TOL, PROJ_TOL, gpu_metrics_torch, orth_err,
+                            projector_distance, rel_residual, residual_bound,
+                            say, to_dev, to_host)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+import paper_2608_28941_amd as rrf  # noqa: E402
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "oracle_configs.json")
+
+
+def _tdt(dtype):
+    return torch.float64 if np.dtype(dtype) == np.float64 else torch.float32
+
+
+def _run(A, w, k_max=0, stop=rrf.RRF_STOP_TRAILING):
+    with rrf.Plan(_tdt(w.dtype), A.shape[0], A.shape[1], w.block_b, k_max) as p:
+        p.set_stop_mode(stop)
+        Q, B, k = p.run(to_dev(A), w.tol, w.block_b, w.sketch_seed)
+        tr = p.trace()
+        st = p.last_status
+        return to_host(Q), to_host(B), k, tr, st
+
+
+def _check_against_live_oracle(w, A, gap=False, elementwise=False):
+    ref = oracle.hbarrf(A, w.tol, w.block_b, w.sketch_seed, dtype=w.np_dtype)
+    say(f"run {w.name} m={w.m} n={w.n} b={w.block_b} tol={w.tol} oracle k={ref.k}")
+    Q, B, k, tr, _ = _run(A, w)
+    assert k == ref.k
+    dt = np.dtype(w.dtype)
+    assert orth_err(Q) <= ORTH_TOL[dt]
+    res_o = rel_residual(A, ref.Q, ref.B)
+    assert rel_residual(A, Q, B) <= residual_bound(res_o, dt)
+    # The per-block stopping quantity follows the oracle's.
+    assert tr["nblocks"] == len(ref.trace)
+    for (kk, e_t, _), g_t in zip(ref.trace, tr["E_trail"]):
+        assert abs(g_t - e_t) <= 1e-3 * max(e_t, 1e-6 * ref.E0) + 1e3 * np.finfo(dt).eps * ref.E0
+    if gap and k > 0:
+        assert projector_distance(Q, ref.Q) <= PROJ_TOL[dt]
+    if elementwise and k > 0:
+        # Q is unique given Omega (Theorem 3.1 + the sign convention); its
+        # columns agree to about cond(A Omega) * u.
+        Om = oracle.normal_v1(w.sketch_seed, A.shape[1], 0, k, dtype=dt).astype(np.float64)
+        sv = np.linalg.svd(A.astype(np.float64) @ Om, compute_uv=False)
+        cond = sv[0] / sv[-1]
+        tol = 1e3 * cond * np.finfo(dt).eps
+        assert np.max(np.abs(Q - ref.Q)) <= tol
+        assert np.max(np.abs(B - ref.B)) <= tol * np.linalg.norm(A, 2)
+    return Q, B, k, ref
+
+
+def test_tiny_config_full_size():
+    w = W.WORKLOADS["tiny_fp64_500x300"]
+    _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
+
+
+SCALED = [
+    ("galore_fp32_4096x4096", 1024, 1024, None, None),
+    ("mlp_fp32_4096x11008", 512, 1376, None, None),
+    ("square_fp64_16384", 2048, 2048, None, 1e-5),
+    ("tall_fp64_131072x2048", 8192, 256, None, None),
+    ("tiny_fp64_500x300", 333, 250, 24, 1e-5),      # b not a power of two
+    ("galore_fp32_4096x4096", 700, 900, 48, 2e-2),  # ragged everywhere
+]
+
+
+@pytest.mark.parametrize("name,m,n,b,tol", SCALED)
+def test_scaled_workloads(name, m, n, b, tol):
+    w = W.scaled(name, m, n, block_b=b, tol=tol)
+    _check_against_live_oracle(w, W.build_matrix(w))
+
+
+@pytest.mark.parametrize("name", W.GAP_INPUTS)
+def test_gap_inputs(name):
+    w = W.WORKLOADS[name]
+    A = W.build_matrix(w)
+    Q, B, k, ref = _check_against_live_oracle(w, A, gap=True)
+    if "exact_rank48" in name:
+        assert k == 48
+    else:
+        assert k == 128
+
+
+def test_wide_and_tall_and_degenerate():
+    for (m, n, b, tol) in [(40, 300, 16, 1e-3), (300, 40, 16, 0.0), (65, 65, 64, 1e-9),
+                           (1, 50, 1, 0.5), (50, 1, 4, 1e-6)]:
+        w = W.Workload(f"edge{m}x{n}", m, n, "float64", b, tol, 5, 6,
+                       kind="lowrank_noise", rank=min(m, n), noise=1e-3,
+                       spectrum="pow10_i_over_30")
+        _check_against_live_oracle(w, W.build_matrix(w))
+    # A = 0 and tol >= 1 give k = 0.
+    with rrf.Plan(torch.float64, 30, 20, 8) as p:
+        Q, B, k = p.run(to_dev(np.zeros((30, 20))), 1e-3, 8, 1)
+        assert k == 0 and Q.shape == (30, 0) and B.shape == (0, 20)
+        A = W.random_dense(30, 20, np.float64, 3)
+        assert p.run(to_dev(A), 1.0, 8, 1)[2] == 0
+
+
+def test_rank_cap_warns_and_tolerance_zero_runs_to_cap():
+    w = W.scaled("tiny_fp64_500x300", 200, 120, block_b=16, tol=1e-9)
+    A = W.build_matrix(w)
+    Q, B, k, _, st = _run(A, w, k_max=40)
+    assert k == 40 and st == rrf.RRF_WARN_KMAX
+    ref = oracle.hbarrf(A, w.tol, 16, w.sketch_seed, k_max=40)
+    assert projector_distance(Q, ref.Q) < 1e-10
+    w0 = W.scaled("tiny_fp64_500x300", 200, 120, block_b=16, tol=0.0)
+    Q, B, k, tr, st = _run(A, w0)
+    assert k == 120 and st == rrf.RRF_OK
+    assert orth_err(Q) <= 1e-12
+
+
+def test_subtract_mode_matches_oracle():
+    w = W.scaled("square_fp64_16384", 1024, 800, block_b=32, tol=1e-4)
+    A = W.build_matrix(w)
+    ref = oracle.hbarrf(A, w.tol, w.block_b, w.sketch_seed, stop="subtract")
+    Q, B, k, tr, _ = _run(A, w, stop=rrf.RRF_STOP_SUBTRACT)
+    assert k == ref.k
+    for (_, _, e_s), g in zip(ref.trace, tr["E_sub"]):
+        assert abs(g - e_s) <= 1e-9 * ref.E0
+
+
+def test_deterministic_repeat():
+    w = W.scaled("galore_fp32_4096x4096", 1024, 768)
+    A = to_dev(W.build_matrix(w))
+    with rrf.Plan(torch.float32, 1024, 768, w.block_b) as p:
+        Q1, B1, k1 = p.run(A, w.tol, w.block_b, w.sketch_seed)
+        Q2, B2, k2 = p.run(A, w.tol, w.block_b, w.sketch_seed)
+        torch.cuda.synchronize()
+        assert k1 == k2
+        assert torch.equal(Q1, Q2) and torch.equal(B1, B2)
+
+
+def test_nonfinite_input_is_an_error():
+    A = W.random_dense(64, 48, np.float64, 9)
+    A[5, 7] = np.nan
+    with rrf.Plan(torch.float64, 64, 48, 16) as p:
+        with pytest.raises(rrf.RRFError) as e:
+            p.run(to_dev(A), 1e-3, 16, 1)
+        assert e.value.status == -3
+
+
+def test_input_is_not_modified():
+    w = W.scaled("square_fp64_16384", 512, 512)
+    A = to_dev(W.build_matrix(w))
+    A0 = A.clone()
+    with rrf.Plan(torch.float64, 512, 512, 64) as p:
+        p.run(A, w.tol, w.block_b, w.sketch_seed)
+    torch.cuda.synchronize()
+    assert torch.equal(A, A0)
+
+
+def test_padded_leading_dimension():
+    w = W.scaled("tiny_fp64_500x300", 300, 200)
+    A = W.build_matrix(w)
+    big = torch.zeros((310, 200), dtype=torch.float64, device="cuda")
+    big = big.t().contiguous().t()
+    big[:300] = torch.from_numpy(A).cuda()
+    view = big[:300]          # lda = 310
+    assert view.stride() == (1, 310)
+    with rrf.Plan(torch.float64, 300, 200, 16) as p:
+        Q, B, k = p.run(view, w.tol, w.block_b, w.sketch_seed)
+    ref = oracle.hbarrf(A, w.tol, w.block_b, w.sketch_seed)
+    assert k == ref.k
+
+
+def _golden():
+    if not os.path.exists(GOLDEN):
+        return {}
+    with open(GOLDEN) as f:
+        return json.load(f)["configs"]
+
+
+@pytest.mark.parametrize("name", W.CONFIGS)
+def test_full_size_config_against_stored_oracle(name):
+    g = _golden().get(name)
+    if g is None:
+        pytest.skip("oracle value not stored for this workload")
+    w = W.WORKLOADS[name]
+    say(f"full-size {name}: building A")
+    A = W.build_matrix(w)
+    Ad = to_dev(A)
+    del A
+    say(f"full-size {name}: rrf_run")
+    with rrf.Plan(_tdt(w.dtype), w.m, w.n, w.block_b) as p:
+        Q, B, k = p.run(Ad, w.tol, w.block_b, w.sketch_seed)
+        tr = p.trace()
+    assert k == g["k"]
+    orth, res = gpu_metrics_torch(Ad, Q, B)
+    dt = np.dtype(w.dtype)
+    assert orth <= ORTH_TOL[dt]
+    assert res <= residual_bound(g["residual_rel"], dt)
+    # The guarantee of Alg. 2 holds at any size.
+    assert res <= w.tol * (1 + 1e-6)
+    # Theorem 3.1 at full size: Q^T A Omega[:, :k] is upper triangular.
+    Om = torch.from_numpy(oracle.normal_v1(w.sketch_seed, w.n, 0, k, dtype=dt)).cuda()
+    R = Q.t().contiguous().to(torch.float64) @ (Ad.to(torch.float64) @ Om.to(torch.float64))
+    low = torch.tril(R, -1).abs().max().item()
+    assert low <= 1e3 * np.finfo(dt).eps * R.abs().max().item()
+    assert tr["nblocks"] == g["blocks"]
