@@ -1,0 +1,196 @@
+"""Benchmark: the range finder on the 16384 x 16384 fp64 workload, one GPU.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--no-cpu-baseline]
+
+A step is one rrf_run (Alg. 2 to the tolerance, then explicit Q and B) with A
+already resident in HBM.  Prints one JSON line:
+  value       algorithmic GFLOP/s of the whole run (flop counts of the method,
+              no padding or speculative work), higher is better;
+  ms_per_step wall time of one run;
+  roofline    the dominant kernel (the fused update) against the fp64 MFMA
+              peak, from HIP events on the plan's stream;
+  gemm_wy     all GEMM-shaped stages together against the same peak;
+  cpu_baseline the CPU oracle on a bounded sample of the same workload.
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"float64": 78.6, "float32": 157.3}   # MI355X dense MFMA
+HBM_GBS = 8000.0
+METRIC = "range-finder wall time (s) + achieved GFLOP/s as % of MFMA peak"
+GEMM_STAGES = ("sample", "reduce", "formw", "update", "orgqr")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="square_fp64_16384")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-steps", type=int, default=3,
+                    help="extra runs with per-kernel HIP-event timing")
+    return ap.parse_args()
+
+
+def algorithmic_flops(m, n, k, b):
+    """Flops the method itself performs for rank k with block b (no padding,
+    no speculative sample of the final block): per block, sample 2 m_i n b_i,
+    block update 4 m_i n b_i + n b_i^2, panel 3 m_i b_i^2 - 2/3 b_i^3; then
+    explicit Q 2 m k^2 - 2/3 k^3."""
+    f = 0.0
+    kk = 0
+    while kk < k:
+        bi = min(b, k - kk)
+        mi = m - kk
+        f += 2.0 * mi * n * bi + 4.0 * mi * n * bi + n * bi * bi
+        f += 3.0 * mi * bi * bi - 2.0 / 3.0 * bi ** 3
+        kk += bi
+    f += 2.0 * m * k * k - 2.0 / 3.0 * k ** 3
+    return f
+
+
+def cpu_baseline(A_host, w, budget_cols=1024, kmax=None):
+    """The oracle (numpy, float64) on a bounded sample: the first block of
+    Alg. 2 on the first ``budget_cols`` columns of the same matrix."""
+    import numpy as np
+    from oracle import hbarrf
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        cores = max((d.get("num_threads", 1) for d in info
+                     if d.get("user_api") == "blas"), default=1)
+    except Exception:
+        cores = os.cpu_count() or 1
+    nc = min(budget_cols, A_host.shape[1])
+    As = np.asfortranarray(A_host[:, :nc])
+    kmax = kmax or w.block_b
+    t0 = time.perf_counter()
+    r = hbarrf(As, 0.0, w.block_b, w.sketch_seed, k_max=kmax, dtype=w.np_dtype)
+    dt = time.perf_counter() - t0
+    fl = algorithmic_flops(As.shape[0], nc, r.k, w.block_b)
+    return {"value": fl / dt / 1e9, "unit": "GFLOP/s", "cores": int(cores),
+            "kind": "oracle", "seconds": dt,
+            "sample": (f"first block (k={r.k}) of Alg. 2 on A[:, :{nc}] of "
+                       f"{w.name} ({As.shape[0]}x{nc}), numpy float64, "
+                       f"one reflector at a time")}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {a.gpus});"
+              " the sharded design is described in DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    import paper_2608_28941_amd as rrf
+    import workloads as W
+
+    w = W.WORKLOADS[a.workload]
+    print(f"[bench] building {w.name} ({w.m}x{w.n} {w.dtype})", file=sys.stderr,
+          flush=True)
+    A_host = W.build_matrix(w)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    A = rrf.colmajor(torch.from_numpy(A_host).to(dev))
+    tdt = torch.float64 if w.dtype == "float64" else torch.float32
+    plan = rrf.Plan(tdt, w.m, w.n, w.block_b)
+
+    def step():
+        return plan.run_raw(A, w.tol, w.block_b, w.sketch_seed)
+
+    print("[bench] warmup", file=sys.stderr, flush=True)
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] timing {a.steps} steps", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        _, _, k, _, _, status = step()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / max(a.steps, 1)
+    tr = plan.trace()
+    flops = algorithmic_flops(w.m, w.n, k, w.block_b)
+
+    # Per-kernel timing (HIP events on the plan's stream) in separate runs.
+    stages = None
+    if a.profile_steps > 0:
+        plan.set_timing(True)
+        acc = {}
+        for _ in range(a.profile_steps):
+            step()
+            for s, v in plan.stage_stats().items():
+                d = acc.setdefault(s, {"ms": 0.0, "launches": 0, "flops": 0.0,
+                                       "bytes": 0.0})
+                for key in d:
+                    d[key] += v[key]
+        plan.set_timing(False)
+        stages = {s: {"ms": v["ms"] / a.profile_steps,
+                      "launches": v["launches"] // a.profile_steps,
+                      "flops": v["flops"] / a.profile_steps,
+                      "bytes": v["bytes"] / a.profile_steps}
+                  for s, v in acc.items()}
+
+    peak = PEAK_TFLOPS[w.dtype]
+    roof = None
+    gemm = None
+    if stages:
+        upd = stages["update"]
+        ach = upd["flops"] / (upd["ms"] * 1e-3) / 1e12 if upd["ms"] > 0 else 0.0
+        roof = {"bound": "mfma", "kernel": "update_kernel (B -= V W, next sample, norms)",
+                "achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(ach / peak, 4), "traffic": None,
+                "avg_launch_ms": upd["ms"] / max(upd["launches"], 1),
+                "launches_per_step": upd["launches"]}
+        gf = sum(stages[s]["flops"] for s in GEMM_STAGES)
+        gm = sum(stages[s]["ms"] for s in GEMM_STAGES)
+        gach = gf / (gm * 1e-3) / 1e12 if gm > 0 else 0.0
+        gemm = {"achieved": round(gach, 3), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(gach / peak, 4), "ms": gm,
+                "stage_ms": {s: round(v["ms"], 4) for s, v in stages.items()}}
+
+    base = None
+    if not a.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle, bounded sample)", file=sys.stderr,
+              flush=True)
+        base = cpu_baseline(A_host, w)
+
+    out = {
+        "metric": METRIC,
+        "value": round(flops / wall / 1e9, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(wall * 1e3, 4),
+        "wall_s": round(wall, 6),
+        "pct_of_mfma_peak": round(100.0 * flops / wall / (peak * 1e12), 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64" if w.dtype == "float64" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "m": w.m, "n": w.n, "block_b": w.block_b,
+                   "tol": w.tol, "k": k, "blocks": tr["nblocks"],
+                   "algorithmic_flops": flops, "status": status,
+                   "matrix_seed": w.matrix_seed, "sketch_seed": w.sketch_seed},
+        "roofline": roof,
+        "gemm_wy": gemm,
+        "cpu_baseline": base,
+    }
+    print(json.dumps(out))
+    plan.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -38,11 +38,12 @@ constexpr int kTLd = 64;          // T stored like geqrt's T: 64 rows
 
 struct Sizes {
   int64_t ldb, kcap, kcols;
-  size_t Bws, V, Tm, tau, Ypart, Om, Zpart, W, Q, Q64, normpart, red, rowj,
-      bar, st, trace;
+  int64_t ldysum;
+  size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
+      rowj, bar, st, trace;
   size_t total() const {
-    return Bws + V + Tm + tau + Ypart + Om + Zpart + W + Q + Q64 + normpart +
-           red + rowj + bar + st + trace;
+    return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
+           normpart + red + rowj + bar + st + trace;
   }
 };
 
@@ -60,6 +61,8 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.Tm = (size_t)kTLd * z.kcols * 8;
   z.tau = (size_t)z.kcols * 8;
   z.Ypart = (size_t)kMaxUpdSplits * z.ldb * 64 * e;
+  z.ldysum = z.ldb + 1024;   // >= the panel grid's padded row count
+  z.Ysum = (size_t)z.ldysum * 64 * 8;
   z.Om = (size_t)n_max * kOmLd * e;
   z.Zpart = (size_t)kMaxRedSplits * n_max * 64 * 8;
   z.W = (size_t)n_max * 64 * 8;
@@ -85,7 +88,7 @@ struct rrf_plan {
   Sizes sz;
   std::vector<void*> dev_allocs;
   void *Bws, *Ypart, *Om, *Zpart, *W, *Q, *Q64;
-  double *V, *Tm, *tau;
+  double *V, *Tm, *tau, *Ysum;
   double *normpart, *red, *rowj, *trace_trail_d, *trace_sub_d;
   unsigned* bar;
   DevState* st;
@@ -294,15 +297,19 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     p->block_start.push_back(k);
     PanelShape sh;
     if (!panel_shape(mp, (int)bi, p->num_cus, p->panel_target, &sh)) return RRF_ERR_SHAPE;
-    PanelArgs<T> pa{};
-    pa.Y = Yp + yoff; pa.ldy = ldb; pa.nsplit = ysplits; pa.split_stride = ldb * 64;
+    RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mp * bi * ysplits + 8.0 * mp * bi,
+               launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
+                                      (int)bi, bp, sh.rows_pad, p->Ysum,
+                                      p->sz.ldysum, s));
+    PanelArgs pa{};
+    pa.Y = p->Ysum; pa.ldy = p->sz.ldysum;
     pa.m = mp; pa.b = (int)bi;
     pa.V = V + k + k * ldb; pa.ldv = ldb;
     pa.Tm = Tm + k * kTLd; pa.ldt = kTLd; pa.tau = tau + k;
     pa.red = p->red; pa.rowj = p->rowj; pa.bar = p->bar; pa.st = p->st; pa.G = sh.G;
     RRF_LAUNCH(p, RRF_STAGE_PANEL,
                2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi,
-               e * 2.0 * mp * bi, launch_panel<T>(pa, sh, s));
+               16.0 * mp * bi, launch_panel(pa, sh, s));
 
     const T* src = blk == 0 ? A : Bws;
     const int64_t lsrc = blk == 0 ? lda : ldb;
@@ -427,13 +434,16 @@ rrf_status panel_stage(rrf_plan* p, const T* Y, int64_t m, int64_t b,
   PanelShape sh;
   if (!panel_shape(m, (int)b, p->num_cus, p->panel_target, &sh)) return RRF_ERR_SHAPE;
   hipStream_t s = p->stream;
-  PanelArgs<T> pa{};
-  pa.Y = Y; pa.ldy = ldy; pa.nsplit = 1; pa.split_stride = 0;
+  hipError_t e0 = launch_gather_panel<T>(Y, ldy, 0, 1, m, (int)b, sh.bp,
+                                         sh.rows_pad, p->Ysum, p->sz.ldysum, s);
+  if (e0 != hipSuccess) return hip_fail(e0);
+  PanelArgs pa{};
+  pa.Y = p->Ysum; pa.ldy = p->sz.ldysum;
   pa.m = m; pa.b = (int)b;
   pa.V = p->V; pa.ldv = p->sz.ldb;
   pa.Tm = p->Tm; pa.ldt = kTLd; pa.tau = p->tau;
   pa.red = p->red; pa.rowj = p->rowj; pa.bar = p->bar; pa.st = p->st; pa.G = sh.G;
-  hipError_t e = launch_panel<T>(pa, sh, s);
+  hipError_t e = launch_panel(pa, sh, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->V, p->sz.ldb, Vout, ldv, m, b, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->Tm, kTLd, Tout, ldt, b, b, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->tau, 1, tauout, 1, b, 1, s);
@@ -541,6 +551,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   RRF_ALLOC(Tm, p->sz.Tm);
   RRF_ALLOC(tau, p->sz.tau);
   RRF_ALLOC(Ypart, p->sz.Ypart);
+  RRF_ALLOC(Ysum, p->sz.Ysum);
   RRF_ALLOC(Om, p->sz.Om);
   RRF_ALLOC(Zpart, p->sz.Zpart);
   RRF_ALLOC(W, p->sz.W);

@@ -21,9 +21,10 @@
 // in the same order, so all derive identical scalars (deterministic, no
 // floating-point atomics).
 //
-// The panel may be float or double; the factorisation always runs in binary64
-// (registers, reductions, V, T, tau), so the reflectors are orthogonal to
-// binary64 precision even for float data.
+// The panel is gathered beforehand into a zero-padded binary64 buffer (the
+// sum of the update's column-split partials); the factorisation runs in
+// binary64 (registers, reductions, V, T, tau), so the reflectors are
+// orthogonal to binary64 precision even for float data.
 //
 // Requires 256 / BP * RPT >= BP so that rows 0 .. b-1 sit in workgroup 0.
 
@@ -34,22 +35,14 @@ namespace {
 
 constexpr unsigned kSpinLimit = 1u << 22;
 
-__device__ __forceinline__ void st_relaxed(double* p, double v) {
-  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p),
-                     (unsigned long long)__double_as_longlong(v),
-                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ double ld_relaxed(const double* p) {
-  const unsigned long long u = __hip_atomic_load(
-      reinterpret_cast<const unsigned long long*>(p), __ATOMIC_RELAXED,
-      __HIP_MEMORY_SCOPE_AGENT);
-  return __longlong_as_double((long long)u);
-}
-
 // Sense-reversing grid barrier (all G workgroups are co-resident: the kernel
-// is launched cooperatively).  The wait is bounded: after kSpinLimit polls it
-// records an error and every later barrier returns at once, so the kernel
-// always drains.
+// is launched cooperatively).  Memory ordering: the partials are written by
+// wave 0 of each workgroup before the barrier; thread 0's agent-scope
+// acquire-release arrival publishes them (it writes back this XCD's L2 and
+// waits for wave 0's stores); after the barrier every wave issues an
+// agent-scope acquire fence before it reads other workgroups' partials.
+// The wait is bounded: after kSpinLimit polls it records an error and every
+// later barrier returns at once, so the kernel always drains.
 __device__ void grid_barrier(unsigned* bar, int G, DevState* st) {
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -81,10 +74,11 @@ __device__ void grid_barrier(unsigned* bar, int G, DevState* st) {
     }
   }
   __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
-template <typename T, int BP, int RPT>
-__global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs<T> a) {
+template <int BP, int RPT>
+__global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs a) {
   constexpr int GR = kPanelThreads / BP;
   constexpr int RW = GR * RPT;
   static_assert(RW >= BP, "rows 0..b-1 must sit in workgroup 0");
@@ -100,16 +94,13 @@ __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs<T> a) {
   const int64_t base = (int64_t)w * RW;
   const int b = a.b;
 
+  // The gathered panel has G * RW rows and BP columns, zero outside (m, b),
+  // so the RPT loads are unconditional and all in flight together.
   double col[RPT];
+  {
+    const double* Yk = a.Y + base + g + (int64_t)k * a.ldy;
 #pragma unroll
-  for (int q = 0; q < RPT; ++q) {
-    const int64_t r = base + g + GR * q;
-    double v = 0.0;
-    if (r < a.m && k < b) {
-      for (int s = 0; s < a.nsplit; ++s)
-        v += (double)a.Y[s * a.split_stride + r + k * a.ldy];
-    }
-    col[q] = v;
+    for (int q = 0; q < RPT; ++q) col[q] = Yk[GR * q];
   }
 
   for (int j = 0; j < b; ++j) {
@@ -136,16 +127,25 @@ __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs<T> a) {
     if (t < BP) {
       double s = 0.0;
       for (int gg = 0; gg < GR; ++gg) s += red_l[gg][t];
-      st_relaxed(&a.red[((int64_t)par * a.G + w) * BP + t], s);
-      if (w == 0) st_relaxed(&a.rowj[par * BP + t], rowj_s[t]);
+      a.red[((int64_t)par * a.G + w) * BP + t] = s;
+      if (w == 0) a.rowj[par * BP + t] = rowj_s[t];
     }
     grid_barrier(a.bar, a.G, a.st);
     // 4. Every workgroup sums all partials in the same fixed order.
     {
       const int kk = t % BP, sub = t / BP;
+      const double* rp = a.red + (int64_t)par * a.G * BP + kk;
       double s = 0.0;
-      for (int ww = sub; ww < a.G; ww += GR)
-        s += ld_relaxed(&a.red[((int64_t)par * a.G + ww) * BP + kk]);
+      for (int w0 = sub; w0 < a.G; w0 += 8 * GR) {
+        double v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int ww = w0 + u * GR;
+          v[u] = ww < a.G ? rp[(int64_t)ww * BP] : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+      }
       red_l[sub][kk] = s;
     }
     __syncthreads();
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs<T> a) {
       double s = 0.0;
       for (int gg = 0; gg < GR; ++gg) s += red_l[gg][t];
       tot[t] = s;
-      rj[t] = ld_relaxed(&a.rowj[par * BP + t]);
+      rj[t] = a.rowj[par * BP + t];
     }
     __syncthreads();
     // 5. dlarfg scalars (identical in every workgroup).
@@ -214,9 +214,23 @@ __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs<T> a) {
   }
 }
 
-template <typename T, int BP, int RPT>
-hipError_t panel_go(const PanelArgs<T>& a, hipStream_t s) {
-  auto fn = panel_kernel<T, BP, RPT>;
+template <typename T>
+__global__ void gather_panel_kernel(const T* P, int64_t ldp, int64_t split_stride,
+                                    int nsplit, int64_t m, int b, int bp,
+                                    int64_t rows_pad, double* Y, int64_t ldy) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= rows_pad) return;
+  for (int k = blockIdx.y; k < bp; k += gridDim.y) {
+    double v = 0.0;
+    if (r < m && k < b)
+      for (int s = 0; s < nsplit; ++s) v += (double)P[s * split_stride + r + k * ldp];
+    Y[r + k * ldy] = v;
+  }
+}
+
+template <int BP, int RPT>
+hipError_t panel_go(const PanelArgs& a, hipStream_t s) {
+  auto fn = panel_kernel<BP, RPT>;
   int occ = 0;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
       &occ, reinterpret_cast<const void*>(fn), kPanelThreads, 0);
@@ -225,20 +239,20 @@ hipError_t panel_go(const PanelArgs<T>& a, hipStream_t s) {
   hipGetDevice(&dev);
   hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (occ < 1 || a.G > occ * cus) return hipErrorCooperativeLaunchTooLarge;
-  PanelArgs<T> arg = a;
+  PanelArgs arg = a;
   void* params[] = {&arg};
   return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(fn),
                                     dim3(a.G), dim3(kPanelThreads), params, 0, s);
 }
 
-template <typename T, int BP>
-hipError_t panel_rpt(const PanelArgs<T>& a, int rpt, hipStream_t s) {
+template <int BP>
+hipError_t panel_rpt(const PanelArgs& a, int rpt, hipStream_t s) {
   switch (rpt) {
-    case 4: if constexpr ((kPanelThreads / BP) * 4 >= BP) return panel_go<T, BP, 4>(a, s); break;
-    case 8: if constexpr ((kPanelThreads / BP) * 8 >= BP) return panel_go<T, BP, 8>(a, s); break;
-    case 16: return panel_go<T, BP, 16>(a, s);
-    case 32: return panel_go<T, BP, 32>(a, s);
-    case 64: return panel_go<T, BP, 64>(a, s);
+    case 4: if constexpr ((kPanelThreads / BP) * 4 >= BP) return panel_go<BP, 4>(a, s); break;
+    case 8: if constexpr ((kPanelThreads / BP) * 8 >= BP) return panel_go<BP, 8>(a, s); break;
+    case 16: return panel_go<BP, 16>(a, s);
+    case 32: return panel_go<BP, 32>(a, s);
+    case 64: return panel_go<BP, 64>(a, s);
   }
   return hipErrorInvalidValue;
 }
@@ -258,24 +272,35 @@ bool panel_shape(int64_t m, int b, int num_cus, int target_wgs, PanelShape* out)
       out->bp = bp;
       out->rpt = rpt;
       out->G = (int)G;
+      out->rows_pad = G * gr * rpt;
       return true;
     }
   }
   return false;
 }
 
-template <typename T>
-hipError_t launch_panel(const PanelArgs<T>& a, const PanelShape& sh,
-                        hipStream_t s) {
+hipError_t launch_panel(const PanelArgs& a, const PanelShape& sh, hipStream_t s) {
   switch (sh.bp) {
-    case 16: return panel_rpt<T, 16>(a, sh.rpt, s);
-    case 32: return panel_rpt<T, 32>(a, sh.rpt, s);
-    case 64: return panel_rpt<T, 64>(a, sh.rpt, s);
+    case 16: return panel_rpt<16>(a, sh.rpt, s);
+    case 32: return panel_rpt<32>(a, sh.rpt, s);
+    case 64: return panel_rpt<64>(a, sh.rpt, s);
   }
   return hipErrorInvalidValue;
 }
 
-template hipError_t launch_panel<float>(const PanelArgs<float>&, const PanelShape&, hipStream_t);
-template hipError_t launch_panel<double>(const PanelArgs<double>&, const PanelShape&, hipStream_t);
+template <typename T>
+hipError_t launch_gather_panel(const T* P, int64_t ldp, int64_t split_stride,
+                               int nsplit, int64_t m, int b, int bp,
+                               int64_t rows_pad, double* Ysum, int64_t ldy,
+                               hipStream_t s) {
+  if (rows_pad <= 0) return hipSuccess;
+  dim3 grid((unsigned)ceil_div(rows_pad, 256), (unsigned)bp);
+  hipLaunchKernelGGL((gather_panel_kernel<T>), grid, dim3(256), 0, s, P, ldp,
+                     split_stride, nsplit, m, b, bp, rows_pad, Ysum, ldy);
+  return hipGetLastError();
+}
+
+template hipError_t launch_gather_panel<float>(const float*, int64_t, int64_t, int, int64_t, int, int, int64_t, double*, int64_t, hipStream_t);
+template hipError_t launch_gather_panel<double>(const double*, int64_t, int64_t, int, int64_t, int, int, int64_t, double*, int64_t, hipStream_t);
 
 }  // namespace rrf

@@ -71,9 +71,9 @@ struct FormWArgs {
   int trans;                   // 1: W = T^T Z,  0: W = T Z
 };
 
-template <typename T>
 struct PanelArgs {
-  const T* Y; int64_t ldy; int nsplit; int64_t split_stride;
+  const double* Y; int64_t ldy;  // gathered panel, zero beyond (m, b), at
+                                 // least G * RW rows and BP columns
   int64_t m; int b;            // panel rows, columns (b <= BP)
   double* V; int64_t ldv;      // m x BP output (binary64 for both dtypes)
   double* Tm; int64_t ldt;     // BP x BP output
@@ -100,11 +100,16 @@ hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s);
 
 // Panel: picks rows-per-thread and grid size; returns hipErrorInvalidValue
 // if the panel does not fit the register-resident capacity.
-struct PanelShape { int bp, rpt, G; };
+struct PanelShape { int bp, rpt, G; int64_t rows_pad; };
 bool panel_shape(int64_t m, int b, int num_cus, int target_wgs, PanelShape* out);
+hipError_t launch_panel(const PanelArgs& a, const PanelShape& sh, hipStream_t s);
+// Ysum[r + k * ldy] = sum_s P_s[r + k * ldp] for r < m, k < b; 0 elsewhere
+// for r < rows_pad, k < bp (binary64).
 template <typename T>
-hipError_t launch_panel(const PanelArgs<T>& a, const PanelShape& sh,
-                        hipStream_t s);
+hipError_t launch_gather_panel(const T* P, int64_t ldp, int64_t split_stride,
+                               int nsplit, int64_t m, int b, int bp,
+                               int64_t rows_pad, double* Ysum, int64_t ldy,
+                               hipStream_t s);
 
 hipError_t launch_finalize(const double* normpart, int nparts, DevState* st,
                            double* trace_trail, double* trace_sub, int block,
