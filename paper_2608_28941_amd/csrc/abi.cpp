@@ -52,7 +52,8 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   (void)b_max;
   Sizes z;
   const size_t e = dt == RRF_F32 ? 4 : 8;
-  z.ldb = round_up(std::max<int64_t>(m_max, 1), 64);
+  // 64 rows of slack: the reduce reads whole 64-row chunks of V.
+  z.ldb = round_up(std::max<int64_t>(m_max, 1), 64) + 64;
   z.kcap = std::min(m_max, n_max);
   if (k_max > 0) z.kcap = std::min(z.kcap, k_max);
   z.kcols = z.kcap + 64;
@@ -63,15 +64,16 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.Ypart = (size_t)kMaxUpdSplits * z.ldb * 64 * e;
   z.ldysum = z.ldb + 1024;   // >= the panel grid's padded row count
   z.Ysum = (size_t)z.ldysum * 64 * 8;
-  z.Om = (size_t)n_max * kOmLd * e;
+  // Omega and W carry zero rows up to the next multiple of the update chunk.
+  z.Om = (size_t)(n_max + kUpdChunk) * kOmLd * e;
   z.Zpart = (size_t)kMaxRedSplits * n_max * 64 * 8;
-  z.W = (size_t)n_max * 64 * 8;
+  z.W = (size_t)(n_max + kUpdChunk) * 64 * 8;
   z.Q = (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * e;
   z.Q64 = dt == RRF_F32 ? (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * 8 : 0;
   z.normpart = (size_t)(ceil_div(m_max, kUpdRows) * kMaxUpdSplits + 1) * 2 * 8;
   z.red = (size_t)2 * kMaxPanelWGs * 64 * 8;
   z.rowj = (size_t)2 * 64 * 8;
-  z.bar = 256;
+  z.bar = (size_t)2 * kMaxPanelWGs * sizeof(unsigned);
   z.st = sizeof(DevState);
   z.trace = (size_t)2 * std::max<int64_t>(z.kcap, 1) * 8;
   return z;
@@ -94,6 +96,7 @@ struct rrf_plan {
   DevState* st;
   DevState* st_host;
   int stop_mode, timing, panel_target;
+  unsigned panel_launches;   // epochs of the panel's publication flags
   // last run
   int64_t last_m, last_n, last_k, last_b, nblocks;
   double E0, sigma2;
@@ -193,6 +196,14 @@ void stats_collect(rrf_plan* p) {
     (p)->bytes[stage] += (by);                             \
   } while (0)
 
+// Epoch base of the next panel launch: a nonzero multiple of 128 (the
+// flags are zeroed at plan creation and a step adds j + 1 <= 64).
+unsigned next_epoch(rrf_plan* p) {
+  p->panel_launches = (p->panel_launches + 1u) & 0x1FFFFFFu;
+  if (p->panel_launches == 0u) p->panel_launches = 1u;
+  return p->panel_launches << 7;
+}
+
 hipError_t read_state(rrf_plan* p) {
   hipError_t e = hipMemcpyAsync(p->st_host, p->st, sizeof(DevState),
                                 hipMemcpyDeviceToHost, p->stream);
@@ -265,7 +276,8 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   const int q0 = b0 > 0 ? pad16(b0) : 0;
   if (b0 > 0)
     RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b0,
-               launch_sketch<T>(seed, n, 0, b0, Om, kOmLd, 1, s));
+               launch_sketch<T>(seed, n, round_up(n, kUpdChunk), 0, b0, Om,
+                                kOmLd, 1, s));
   UpdateArgs<T> u{};
   u.src = A; u.lds = lda; u.dst = nullptr; u.ldd = 0; u.mr = m; u.n = n;
   u.V = nullptr; u.ldv = 0; u.bp = 0; u.W = nullptr; u.ldw = 0;
@@ -306,7 +318,8 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     pa.m = mp; pa.b = (int)bi;
     pa.V = V + k + k * ldb; pa.ldv = ldb;
     pa.Tm = Tm + k * kTLd; pa.ldt = kTLd; pa.tau = tau + k;
-    pa.red = p->red; pa.rowj = p->rowj; pa.bar = p->bar; pa.st = p->st; pa.G = sh.G;
+    pa.red = p->red; pa.rowj = p->rowj; pa.flags = p->bar; pa.st = p->st; pa.G = sh.G;
+    pa.epoch_base = next_epoch(p);
     RRF_LAUNCH(p, RRF_STAGE_PANEL,
                2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi,
                16.0 * mp * bi, launch_panel(pa, sh, s));
@@ -337,7 +350,8 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     const int q_next = b_next > 0 ? pad16(b_next) : 0;
     if (b_next > 0)
       RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
-                 launch_sketch<T>(seed, n, k_next, b_next, Om, kOmLd, 1, s));
+                 launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_next,
+                                  b_next, Om, kOmLd, 1, s));
 
     // B[k:m, :] -= V_i W, fused with the next sample and the norms.
     UpdateArgs<T> ua{};
@@ -442,7 +456,8 @@ rrf_status panel_stage(rrf_plan* p, const T* Y, int64_t m, int64_t b,
   pa.m = m; pa.b = (int)b;
   pa.V = p->V; pa.ldv = p->sz.ldb;
   pa.Tm = p->Tm; pa.ldt = kTLd; pa.tau = p->tau;
-  pa.red = p->red; pa.rowj = p->rowj; pa.bar = p->bar; pa.st = p->st; pa.G = sh.G;
+  pa.red = p->red; pa.rowj = p->rowj; pa.flags = p->bar; pa.st = p->st; pa.G = sh.G;
+  pa.epoch_base = next_epoch(p);
   hipError_t e = launch_panel(pa, sh, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->V, p->sz.ldb, Vout, ldv, m, b, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->Tm, kTLd, Tout, ldt, b, b, s);
@@ -518,6 +533,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   p->stop_mode = RRF_STOP_TRAILING;
   p->timing = 0;
   p->panel_target = 64;
+  p->panel_launches = 0;
   if (const char* pt = std::getenv("RRF_PANEL_WGS")) {
     const int v = std::atoi(pt);
     if (v >= 1 && v <= kMaxPanelWGs) p->panel_target = v;
@@ -635,7 +651,7 @@ rrf_status rrf_run(rrf_plan_t plan, const void* A, int64_t m, int64_t n,
     if (st != RRF_OK) {
       (void)hipStreamSynchronize(plan->stream);
       if (plan->st_host && plan->st_host->barrier_err) {
-        (void)launch_zero_u32(plan->bar, 2, plan->stream);
+        (void)launch_zero_u32(plan->bar, 2 * kMaxPanelWGs, plan->stream);
         (void)hipStreamSynchronize(plan->stream);
       }
       plan->nblocks = 0;
@@ -717,10 +733,10 @@ rrf_status rrf_sketch(rrf_dtype dtype, uint64_t seed, int64_t n, int64_t col0,
   if (n == 0 || ncols == 0) return RRF_OK;
   hipError_t e;
   if (dtype == RRF_F64)
-    e = launch_sketch<double>(seed, n, col0, ncols, (double*)out, 1, ldo,
+    e = launch_sketch<double>(seed, n, n, col0, ncols, (double*)out, 1, ldo,
                               (hipStream_t)hip_stream);
   else
-    e = launch_sketch<float>(seed, n, col0, ncols, (float*)out, 1, ldo,
+    e = launch_sketch<float>(seed, n, n, col0, ncols, (float*)out, 1, ldo,
                              (hipStream_t)hip_stream);
   return e == hipSuccess ? RRF_OK : hip_fail(e);
 }

@@ -33,48 +33,63 @@
 namespace rrf {
 namespace {
 
-constexpr unsigned kSpinLimit = 1u << 22;
+constexpr unsigned kSpinLimit = 1u << 24;
 
-// Sense-reversing grid barrier (all G workgroups are co-resident: the kernel
-// is launched cooperatively).  Memory ordering: the partials are written by
-// wave 0 of each workgroup before the barrier; thread 0's agent-scope
-// acquire-release arrival publishes them (it writes back this XCD's L2 and
-// waits for wave 0's stores); after the barrier every wave issues an
-// agent-scope acquire fence before it reads other workgroups' partials.
-// The wait is bounded: after kSpinLimit polls it records an error and every
-// later barrier returns at once, so the kernel always drains.
-__device__ void grid_barrier(unsigned* bar, int G, DevState* st) {
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    if (__hip_atomic_load(&st->barrier_err, __ATOMIC_RELAXED,
-                          __HIP_MEMORY_SCOPE_AGENT) == 0) {
-      const unsigned gen = __hip_atomic_load(&bar[1], __ATOMIC_ACQUIRE,
-                                             __HIP_MEMORY_SCOPE_AGENT);
-      const unsigned arrived = __hip_atomic_fetch_add(
-          &bar[0], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-      if (arrived == (unsigned)G - 1u) {
-        __hip_atomic_store(&bar[0], 0u, __ATOMIC_RELAXED,
+// Cross-workgroup traffic uses agent-scope atomic accesses only (coherent
+// across the XCDs without L2 write-back or invalidation, which an
+// agent-scope fence would cost on every step).
+//
+// Publication: wave 0 of workgroup w stores its partials with agent-scope
+// relaxed stores, waits until they have completed (s_waitcnt vmcnt(0)), then
+// stores flags[par][w] = epoch.  A reader waits, one lane per flag, until
+// every flag of the step carries the step's epoch, then reads the partials
+// with agent-scope loads issued after the wait.  Epochs are unique per launch
+// and step, so flags left by earlier launches never match.  The wait is
+// bounded: after kSpinLimit polls it records an error and every later wait
+// returns at once, so the kernel always drains.
+__device__ __forceinline__ void st_agent(double* p, double v) {
+  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p),
+                     (unsigned long long)__double_as_longlong(v),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_agent(const double* p) {
+  const unsigned long long u = __hip_atomic_load(
+      reinterpret_cast<const unsigned long long*>(p), __ATOMIC_RELAXED,
+      __HIP_MEMORY_SCOPE_AGENT);
+  return __longlong_as_double((long long)u);
+}
+
+// s_waitcnt vmcnt(0) with expcnt and lgkmcnt left at their maxima (gfx9
+// encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[15:14]).
+constexpr unsigned kWaitVmcnt0 = 0x0F70;
+
+__device__ __forceinline__ void publish(unsigned* flag, unsigned epoch) {
+  if (threadIdx.x < 64) {
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    if (threadIdx.x == 0)
+      __hip_atomic_store(flag, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+__device__ __forceinline__ void wait_all(const unsigned* flags, int G,
+                                         unsigned epoch, DevState* st) {
+  if ((int)threadIdx.x < G) {
+    unsigned spins = 0;
+    while (__hip_atomic_load(&flags[threadIdx.x], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT) != epoch) {
+      __builtin_amdgcn_s_sleep(1);
+      ++spins;
+      if ((spins & 255u) == 0u &&
+          (spins > kSpinLimit ||
+           __hip_atomic_load(&st->barrier_err, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT) != 0)) {
+        __hip_atomic_store(&st->barrier_err, 1, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&bar[1], gen + 1u, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
-      } else {
-        unsigned spins = 0;
-        while (__hip_atomic_load(&bar[1], __ATOMIC_ACQUIRE,
-                                 __HIP_MEMORY_SCOPE_AGENT) == gen) {
-          __builtin_amdgcn_s_sleep(1);
-          if (++spins > kSpinLimit ||
-              __hip_atomic_load(&st->barrier_err, __ATOMIC_RELAXED,
-                                __HIP_MEMORY_SCOPE_AGENT) != 0) {
-            __hip_atomic_store(&st->barrier_err, 1, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-            break;
-          }
-        }
+        break;
       }
     }
   }
   __syncthreads();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
 template <int BP, int RPT>
@@ -87,6 +102,8 @@ __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs a) {
   __shared__ double red_l[GR][BP];
   __shared__ double tot[BP], rj[BP];
   __shared__ double Tl[BP][BP + 1];
+  __shared__ double Ej[BP];          // v_p^T v_j, p < j, of the last step
+  __shared__ double tau_s[BP];
 
   const int t = threadIdx.x;
   const int k = t % BP, g = t / BP;
@@ -103,57 +120,88 @@ __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs a) {
     for (int q = 0; q < RPT; ++q) col[q] = Yk[GR * q];
   }
 
+  // Column jj of T (workgroup 0) from Ej and tau_s: the forward columnwise
+  // recursion T[:jj, jj] = -tau_jj T[:jj, :jj] (V^T v_jj).
+  auto t_column = [&](int jj) {
+    if (t < jj) {
+      double acc = 0.0;
+      for (int p = t; p < jj; ++p) acc += Tl[t][p] * Ej[p];
+      Tl[t][jj] = -tau_s[jj] * acc;
+    } else if (t == jj) {
+      Tl[jj][jj] = tau_s[jj];
+    }
+  };
+
   for (int j = 0; j < b; ++j) {
     const int par = j & 1;
-    // 1. Broadcast column j (rows of this workgroup) and row j.
+    // 1. Broadcast column j with its rows <= j zeroed: then every dot below
+    //    is over rows > j and the rank-1 update leaves rows <= j untouched,
+    //    with no per-row conditions.  Row j of every column sits in
+    //    workgroup 0 (row group j % GR, register j / GR).
+    constexpr int QJ = (BP + GR - 1) / GR;   // registers that can hold rows < BP
     if (k == j) {
+      if (w == 0) {
 #pragma unroll
-      for (int q = 0; q < RPT; ++q) xs[g + GR * q] = col[q];
+        for (int q = 0; q < RPT; ++q)
+          xs[g + GR * q] = (q < QJ && g + GR * q <= j) ? 0.0 : col[q];
+      } else {
+#pragma unroll
+        for (int q = 0; q < RPT; ++q) xs[g + GR * q] = col[q];
+      }
     }
+    if (w == 0 && g == j % GR) {
+      const int qj = j / GR;
+      double v = 0.0;
 #pragma unroll
-    for (int q = 0; q < RPT; ++q)
-      if (base + g + GR * q == j) rowj_s[k] = col[q];
+      for (int q = 0; q < QJ; ++q) v = (q == qj) ? col[q] : v;
+      rowj_s[k] = v;
+    }
     __syncthreads();
-    // 2. Partial dot of this thread's column with x over rows > j.
+    // 2. Partial dot of this thread's column with x (rows > j).
     double d = 0.0;
 #pragma unroll
-    for (int q = 0; q < RPT; ++q) {
-      const int64_t r = base + g + GR * q;
-      if (r > j && r < a.m) d += col[q] * xs[g + GR * q];
-    }
+    for (int q = 0; q < RPT; ++q) d += col[q] * xs[g + GR * q];
     red_l[g][k] = d;
     __syncthreads();
-    // 3. Workgroup partial to global memory.
+    // 3. Workgroup partial to global memory (wave 0), then publish.  While
+    //    the other workgroups catch up, workgroup 0 finishes the previous
+    //    column of T.
+    const unsigned epoch = a.epoch_base + (unsigned)j + 1u;
     if (t < BP) {
       double s = 0.0;
       for (int gg = 0; gg < GR; ++gg) s += red_l[gg][t];
-      a.red[((int64_t)par * a.G + w) * BP + t] = s;
-      if (w == 0) a.rowj[par * BP + t] = rowj_s[t];
+      st_agent(&a.red[((int64_t)par * a.G + w) * BP + t], s);
+      if (w == 0) st_agent(&a.rowj[par * BP + t], rowj_s[t]);
     }
-    grid_barrier(a.bar, a.G, a.st);
-    // 4. Every workgroup sums all partials in the same fixed order.
+    publish(&a.flags[par * kMaxPanelWGs + w], epoch);
+    if (w == 0 && j > 0) t_column(j - 1);
+    wait_all(a.flags + par * kMaxPanelWGs, a.G, epoch, a.st);
+    // 4. Every workgroup sums all partials in the same fixed order; row j is
+    //    loaded in the same batch.
     {
       const int kk = t % BP, sub = t / BP;
       const double* rp = a.red + (int64_t)par * a.G * BP + kk;
+      const double rjv = (t < BP) ? ld_agent(&a.rowj[par * BP + t]) : 0.0;
       double s = 0.0;
-      for (int w0 = sub; w0 < a.G; w0 += 8 * GR) {
-        double v[8];
+      for (int w0 = sub; w0 < a.G; w0 += 16 * GR) {
+        double v[16];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < 16; ++u) {
           const int ww = w0 + u * GR;
-          v[u] = ww < a.G ? rp[(int64_t)ww * BP] : 0.0;
+          v[u] = ld_agent(&rp[(int64_t)(ww < a.G ? ww : 0) * BP]);
         }
 #pragma unroll
-        for (int u = 0; u < 8; ++u) s += v[u];
+        for (int u = 0; u < 16; ++u)
+          if (w0 + u * GR < a.G) s += v[u];
       }
       red_l[sub][kk] = s;
+      if (t < BP) rj[t] = rjv;
     }
     __syncthreads();
     if (t < BP) {
       double s = 0.0;
       for (int gg = 0; gg < GR; ++gg) s += red_l[gg][t];
       tot[t] = s;
-      rj[t] = a.rowj[par * BP + t];
     }
     __syncthreads();
     // 5. dlarfg scalars (identical in every workgroup).
@@ -166,34 +214,26 @@ __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs a) {
       tau_j = (beta - alpha) / beta;
       scale = 1.0 / (alpha - beta);
     }
-    // 6. v_j = x * scale below the diagonal; trailing columns
-    //    y_k -= tau_j (v_j^T y_k) v_j with v_j^T y_k = y_k[j] + scale * dot_k.
+    // 6. v_j = x * scale below the diagonal (rows <= j of column j are never
+    //    read again); trailing columns y_k -= tau_j (v_j^T y_k) v_j with
+    //    v_j^T y_k = y_k[j] + scale * dot_k (xs is zero on rows <= j).
     if (k == j) {
 #pragma unroll
-      for (int q = 0; q < RPT; ++q) {
-        const int64_t r = base + g + GR * q;
-        if (r > j) col[q] = col[q] * scale;
-      }
+      for (int q = 0; q < RPT; ++q) col[q] = col[q] * scale;
     } else if (k > j && k < b) {
-      const double f = tau_j * (rj[k] + scale * tot[k]);
+      const double fs = tau_j * (rj[k] + scale * tot[k]) * scale;
 #pragma unroll
-      for (int q = 0; q < RPT; ++q) {
-        const int64_t r = base + g + GR * q;
-        if (r > j) col[q] = col[q] - f * (xs[g + GR * q] * scale);
-      }
+      for (int q = 0; q < RPT; ++q) col[q] = col[q] - fs * xs[g + GR * q];
     }
-    // 7. Column j of T (workgroup 0): v_p^T v_j = V[j, p] + scale * dot_p.
+    // 7. Save v_p^T v_j = V[j, p] + scale * dot_p (p < j) for T (workgroup 0).
     if (w == 0) {
-      if (t < j) {
-        double acc = 0.0;
-        for (int p = t; p < j; ++p) acc += Tl[t][p] * (rj[p] + scale * tot[p]);
-        Tl[t][j] = -tau_j * acc;
-      } else if (t == j) {
-        Tl[j][j] = tau_j;
-      }
+      if (t < j) Ej[t] = rj[t] + scale * tot[t];
+      else if (t == j) tau_s[j] = tau_j;
     }
     __syncthreads();
   }
+  if (w == 0 && b > 0) t_column(b - 1);
+  __syncthreads();
 
   // Outputs: V with explicit unit diagonal and zeros above / beyond b.
 #pragma unroll

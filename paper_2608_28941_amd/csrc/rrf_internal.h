@@ -80,17 +80,19 @@ struct PanelArgs {
   double* tau;                 // b outputs
   double* red;                 // 2 x G x BP
   double* rowj;                // 2 x BP
-  unsigned* bar;               // {count, generation}
+  unsigned* flags;             // 2 x kMaxPanelWGs publication flags
+  unsigned epoch_base;         // unique per launch, multiple of 128, > 0
   DevState* st;
   int G;
 };
 
 // Launchers (return hipError_t of the launch) ------------------------------
 
+// Rows [n, n_pad) of the output are written as zeros.
 template <typename T>
-hipError_t launch_sketch(uint64_t seed, int64_t n, int64_t col0, int64_t ncols,
-                         T* out, int64_t row_stride, int64_t col_stride,
-                         hipStream_t s);
+hipError_t launch_sketch(uint64_t seed, int64_t n, int64_t n_pad, int64_t col0,
+                         int64_t ncols, T* out, int64_t row_stride,
+                         int64_t col_stride, hipStream_t s);
 template <typename T>
 hipError_t launch_update(const UpdateArgs<T>& a, int nsplit, hipStream_t s);
 template <typename T>

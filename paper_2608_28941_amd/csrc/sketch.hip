@@ -120,13 +120,21 @@ __device__ __forceinline__ void box_muller(uint64_t wa, uint64_t wb,
   *z1 = r * cs.s;
 }
 
+// Rows [n, n_pad) are written as zeros (the update stages whole chunks).
 template <typename T>
 __global__ __launch_bounds__(256) void sketch_kernel(
-    uint64_t seed, int64_t n, int64_t col0, int64_t ncols, T* out,
-    int64_t row_stride, int64_t col_stride) {
+    uint64_t seed, int64_t n, int64_t n_pad, int64_t col0, int64_t ncols,
+    T* out, int64_t row_stride, int64_t col_stride) {
   const int64_t nq = (n + 3) / 4;
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= nq) return;
+  if (q >= nq) {
+    const int64_t r0 = 4 * q;
+    if (r0 < n_pad)
+      for (int64_t j = blockIdx.y; j < ncols; j += gridDim.y)
+        for (int t = 0; t < 4; ++t)
+          if (r0 + t < n_pad) out[(r0 + t) * row_stride + j * col_stride] = T(0);
+    return;
+  }
   for (int64_t j = blockIdx.y; j < ncols; j += gridDim.y) {
     const uint64_t g = (uint64_t)(col0 + j);
     uint64_t w[4];
@@ -138,6 +146,7 @@ __global__ __launch_bounds__(256) void sketch_kernel(
     for (int t = 0; t < 4; ++t) {
       const int64_t r = 4 * q + t;
       if (r < n) out[r * row_stride + j * col_stride] = (T)z[t];
+      else if (r < n_pad) out[r * row_stride + j * col_stride] = T(0);
     }
   }
 }
@@ -145,20 +154,23 @@ __global__ __launch_bounds__(256) void sketch_kernel(
 }  // namespace
 
 template <typename T>
-hipError_t launch_sketch(uint64_t seed, int64_t n, int64_t col0, int64_t ncols,
-                         T* out, int64_t row_stride, int64_t col_stride,
-                         hipStream_t s) {
+hipError_t launch_sketch(uint64_t seed, int64_t n, int64_t n_pad, int64_t col0,
+                         int64_t ncols, T* out, int64_t row_stride,
+                         int64_t col_stride, hipStream_t s) {
   if (n <= 0 || ncols <= 0) return hipSuccess;
-  const int64_t nq = (n + 3) / 4;
+  if (n_pad < n) n_pad = n;
+  const int64_t nq = (n_pad + 3) / 4;
   dim3 grid((unsigned)ceil_div(nq, 256), (unsigned)(ncols < 65535 ? ncols : 65535));
-  hipLaunchKernelGGL(sketch_kernel<T>, grid, dim3(256), 0, s, seed, n, col0,
-                     ncols, out, row_stride, col_stride);
+  hipLaunchKernelGGL(sketch_kernel<T>, grid, dim3(256), 0, s, seed, n, n_pad,
+                     col0, ncols, out, row_stride, col_stride);
   return hipGetLastError();
 }
 
 template hipError_t launch_sketch<float>(uint64_t, int64_t, int64_t, int64_t,
-                                         float*, int64_t, int64_t, hipStream_t);
+                                         int64_t, float*, int64_t, int64_t,
+                                         hipStream_t);
 template hipError_t launch_sketch<double>(uint64_t, int64_t, int64_t, int64_t,
-                                          double*, int64_t, int64_t, hipStream_t);
+                                          int64_t, double*, int64_t, int64_t,
+                                          hipStream_t);
 
 }  // namespace rrf

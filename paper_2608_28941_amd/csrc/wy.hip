@@ -46,37 +46,63 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs<T> a) {
   const bool colok = col < a.n;
   const int64_t r_begin = (int64_t)blockIdx.y * a.rows_per_split;
   const int64_t r_end = min(a.mr, r_begin + a.rows_per_split);
-  const T* Xc = a.X + (colok ? col : 0) * a.ldx;
+  const T* Xc = a.X + (colok ? col : a.n - 1) * a.ldx;
 
   acc_t acc[NPT];
 #pragma unroll
   for (int pt = 0; pt < NPT; ++pt) acc[pt] = Mfma<T>::zero();
 
+  // Loads are unconditional from clamped in-bounds addresses; rows past
+  // r_end are cancelled by zero V rows (mask multiply, so the compiler
+  // cannot turn the loads into branches), columns past n are not stored.
+  // The next chunk's X values are loaded while the current chunk computes.
+  const int64_t rlast = a.mr - 1;
+  constexpr int NX = kRedChunk / 4;   // X values per lane per chunk
+  T xcur[NX], xnxt[NX];
+#pragma unroll
+  for (int u = 0; u < NX; ++u) {
+    const int64_t r = r_begin + (u / 4) * 16 + 4 * (u % 4) + g;
+    xcur[u] = Xc[r < a.mr ? r : rlast];
+  }
   for (int64_t R = r_begin; R < r_end; R += kRedChunk) {
     __syncthreads();
-    for (int idx = threadIdx.x; idx < BP * kRedChunk; idx += 256) {
-      const int rr = idx % kRedChunk, p = idx / kRedChunk;
+    {
+      // V rows of this chunk: all loads, then the next chunk's X loads, then
+      // the LDS writes (which wait for the V loads only).
+      constexpr int NIT = (BP * kRedChunk) / 256;
+      const int rr = threadIdx.x % kRedChunk;
+      const int p0 = threadIdx.x / kRedChunk;
       const int64_t r = R + rr;
-      vl[p * LDV + rr] = (r < r_end) ? (T)a.V[r + p * a.ldv] : T(0);
-    }
-    __syncthreads();
-    const int64_t rows_here = min((int64_t)kRedChunk, r_end - R);
-    for (int s16 = 0; s16 < rows_here; s16 += 16) {
-      T xa[4];
+      const double mask = r < r_end ? 1.0 : 0.0;
+      const double* Vr = a.V + (r < r_end ? r : rlast);
+      double tmp[NIT];
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int64_t r = R + s16 + 4 * s + g;
-        xa[s] = (colok && r < r_end) ? Xc[r] : T(0);
+      for (int it = 0; it < NIT; ++it) tmp[it] = Vr[(int64_t)(p0 + 4 * it) * a.ldv];
+      if (R + kRedChunk < r_end) {
+#pragma unroll
+        for (int u = 0; u < NX; ++u) {
+          const int64_t rx = R + kRedChunk + (u / 4) * 16 + 4 * (u % 4) + g;
+          xnxt[u] = Xc[rx < a.mr ? rx : rlast];
+        }
       }
 #pragma unroll
+      for (int it = 0; it < NIT; ++it) vl[(p0 + 4 * it) * LDV + rr] = (T)(mask * tmp[it]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int sl = 0; sl < kRedChunk / 16; ++sl) {
+#pragma unroll
       for (int s = 0; s < 4; ++s) {
+        const T xa = xcur[sl * 4 + s];
 #pragma unroll
         for (int pt = 0; pt < NPT; ++pt) {
-          const T bv = vl[(pt * 16 + m16) * LDV + s16 + 4 * s + g];
-          acc[pt] = Mfma<T>::op(xa[s], bv, acc[pt]);
+          const T bv = vl[(pt * 16 + m16) * LDV + sl * 16 + 4 * s + g];
+          acc[pt] = Mfma<T>::op(xa, bv, acc[pt]);
         }
       }
     }
+#pragma unroll
+    for (int u = 0; u < NX; ++u) xcur[u] = xnxt[u];
   }
   // Lane holds Z^T[c = cb + drow(g, i)][p = pt * 16 + m16].
   T* Z = a.Z + (int64_t)blockIdx.y * a.split_stride;
@@ -105,7 +131,10 @@ __global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
     Tl[i][j] = (i <= j && j < a.b) ? a.Tm[i + j * a.ldt] : 0.0;
   }
   const int p = threadIdx.x % BP, cl = threadIdx.x / BP;
-  for (int64_t c0 = (int64_t)blockIdx.x * CPB; c0 < a.n;
+  // Rows [n, round_up(n, kUpdChunk)) of W are written as zeros so the update
+  // can stage whole chunks without predicates.
+  const int64_t n_pad = (a.n + kUpdChunk - 1) / kUpdChunk * kUpdChunk;
+  for (int64_t c0 = (int64_t)blockIdx.x * CPB; c0 < n_pad;
        c0 += (int64_t)gridDim.x * CPB) {
     __syncthreads();
     const int64_t c = c0 + cl;
@@ -121,7 +150,7 @@ __global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
     } else {
       for (int l = p; l < BP; ++l) w += Tl[p][l] * zs[cl][l];
     }
-    if (c < a.n) a.W[c * BP + p] = (T)w;
+    if (c < n_pad) a.W[c * BP + p] = (T)w;
   }
 }
 
@@ -150,9 +179,12 @@ __global__ __launch_bounds__(256) void update_kernel(UpdateArgs<T> a) {
 
   // This wavefront's slice of -V^T as MFMA B operands: B[g][m] = -V[r][4 p4 + g].
   T vreg[NP4 > 0 ? NP4 : 1];
+  {
+    const double vmask = rowok ? -1.0 : 0.0;   // mask multiply keeps the loads batched
 #pragma unroll
-  for (int p4 = 0; p4 < NP4; ++p4)
-    vreg[p4] = rowok ? -(T)a.V[rr + (4 * p4 + g) * a.ldv] : T(0);
+    for (int p4 = 0; p4 < NP4; ++p4)
+      vreg[p4] = (T)(vmask * a.V[rr + (4 * p4 + g) * a.ldv]);
+  }
 
   acc_t pacc[NQT > 0 ? NQT : 1];
 #pragma unroll
@@ -160,25 +192,62 @@ __global__ __launch_bounds__(256) void update_kernel(UpdateArgs<T> a) {
   double nb = 0.0, nt = 0.0;
   const bool in_block = r < a.s0;
 
+  // Staging values (W, Omega) and B tiles of the next chunk are loaded into
+  // registers while the current chunk computes.  Chunks start at multiples
+  // of kUpdChunk and split boundaries are multiples of kUpdChunk, so a chunk
+  // only runs past ce at the end of the matrix, where W and Omega carry zero
+  // rows up to the next multiple; B loads use clamped in-bounds addresses
+  // (invalid rows are never stored and add nothing to the norms; invalid
+  // columns only occur past n, where the staged W and Omega rows are zero).
+  constexpr int NW = BP > 0 ? (kUpdChunk * BP) / 256 : 0;
+  constexpr int NO = (kUpdChunk * QP) / 256;
+  constexpr int NCT = kUpdChunk / 16;
+  static_assert((kUpdChunk * BP) % 256 == 0 && (kUpdChunk * QP) % 256 == 0,
+                "chunk staging assumes whole passes of 256 threads");
+  T tw[NW > 0 ? NW : 1], to[NO > 0 ? NO : 1];
+  T bx[NCT][4];
+  auto load_chunk = [&](int64_t cc0) {
+#pragma unroll
+    for (int it = 0; it < NW; ++it) {
+      const int idx = threadIdx.x + 256 * it;
+      tw[it] = a.W[(cc0 + idx / BP) * a.ldw + idx % BP];
+    }
+#pragma unroll
+    for (int it = 0; it < NO; ++it) {
+      const int idx = threadIdx.x + 256 * it;
+      to[it] = a.Om[(cc0 + idx / QP) * a.ldo + idx % QP];
+    }
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t c = cc0 + ct * 16 + Mfma<T>::drow(g, i);
+        bx[ct][i] = a.src[rr + (c < a.n ? c : a.n - 1) * a.lds];
+      }
+  };
+  if (cs < ce) load_chunk(cs);
+
   for (int64_t c0 = cs; c0 < ce; c0 += kUpdChunk) {
     __syncthreads();
-    if (BP > 0) {
-      for (int idx = threadIdx.x; idx < kUpdChunk * BP; idx += 256) {
-        const int p = idx % BP, cc = idx / BP;
-        const int64_t c = c0 + cc;
-        wl[cc * LDW + p] = (c < ce) ? a.W[c * a.ldw + p] : T(0);
-      }
+#pragma unroll
+    for (int it = 0; it < NW; ++it) {
+      const int idx = threadIdx.x + 256 * it;
+      wl[(idx / BP) * LDW + idx % BP] = tw[it];
     }
-    if (QP > 0) {
-      for (int idx = threadIdx.x; idx < kUpdChunk * QP; idx += 256) {
-        const int q = idx % QP, cc = idx / QP;
-        const int64_t c = c0 + cc;
-        ol[cc * LDO + q] = (c < ce) ? a.Om[c * a.ldo + q] : T(0);
-      }
+#pragma unroll
+    for (int it = 0; it < NO; ++it) {
+      const int idx = threadIdx.x + 256 * it;
+      ol[(idx / QP) * LDO + idx % QP] = to[it];
     }
     __syncthreads();
+    T bcur[NCT][4];
 #pragma unroll
-    for (int ct = 0; ct < kUpdChunk / 16; ++ct) {
+    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) bcur[ct][i] = bx[ct][i];
+    if (c0 + kUpdChunk < ce) load_chunk(c0 + kUpdChunk);
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
       // D[M = column drow(g, i)][N = row m16] of this 16 x 16 tile.
       acc_t acc;
       bool cok[4];
@@ -186,7 +255,7 @@ __global__ __launch_bounds__(256) void update_kernel(UpdateArgs<T> a) {
       for (int i = 0; i < 4; ++i) {
         const int64_t c = c0 + ct * 16 + Mfma<T>::drow(g, i);
         cok[i] = c < ce;
-        acc[i] = (rowok && cok[i]) ? a.src[rr + c * a.lds] : T(0);
+        acc[i] = bcur[ct][i];
       }
 #pragma unroll
       for (int p4 = 0; p4 < NP4; ++p4) {
