@@ -2,6 +2,9 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline]
+    python bench.py --copy-probe MIB      one plain device copy of MIB MiB
+                                          (calibrates the HBM byte counters)
+    python bench.py --summarize DIR...    per-kernel summary of rocprofv3 CSVs
 
 A step is one rrf_run (Alg. 2 to the tolerance, then explicit Q and B) with A
 already resident in HBM.  Prints one JSON line:
@@ -16,8 +19,8 @@ already resident in HBM.  Prints one JSON line:
 
 import argparse
 import json
-import math
 import os
+import re
 import sys
 import time
 
@@ -39,7 +42,95 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=3,
                     help="extra runs with per-kernel HIP-event timing")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run one device-to-device copy of MIB MiB")
+    ap.add_argument("--summarize", nargs="+", default=None, metavar="DIR",
+                    help="only summarise rocprofv3 CSV output (no GPU)")
     return ap.parse_args()
+
+
+def short_kernel(name):
+    """'void rrf::(anonymous namespace)::update_kernel<double, 64, 64>(...)'
+    -> 'update_kernel<double, 64, 64>'."""
+    name = re.sub(r"^void\s+", "", name)
+    name = name.replace("rrf::(anonymous namespace)::", "").replace("rrf::", "")
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0 and i > 0:
+            return name[:i]
+    return name
+
+
+def summarize(dirs):
+    """Markdown tables of the kernel-trace statistics and of the per-dispatch
+    counter values (mean over dispatches) found under ``dirs``."""
+    import csv
+    import glob
+    lines = []
+    for d in dirs:
+        for f in sorted(glob.glob(os.path.join(d, "**", "*kernel_stats.csv"),
+                                  recursive=True)):
+            lines.append(f"### kernel statistics ({os.path.basename(f)})\n")
+            lines.append("| kernel | calls | total ms | avg us | min us | max us | % |")
+            lines.append("|---|---:|---:|---:|---:|---:|---:|")
+            for r in csv.DictReader(open(f)):
+                lines.append("| {} | {} | {:.3f} | {:.1f} | {:.1f} | {:.1f} | {} |".format(
+                    short_kernel(r["Name"]), r["Calls"],
+                    float(r["TotalDurationNs"]) / 1e6, float(r["AverageNs"]) / 1e3,
+                    float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, r["Percentage"]))
+            lines.append("")
+        for f in sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"),
+                                  recursive=True)):
+            acc = {}
+            disp = {}
+            for r in csv.DictReader(open(f)):
+                k = short_kernel(r["Kernel_Name"])
+                c = r["Counter_Name"]
+                key = (k, c)
+                acc.setdefault(key, {})
+                did = r["Dispatch_Id"]
+                acc[key][did] = acc[key].get(did, 0.0) + float(r["Counter_Value"])
+                disp.setdefault(k, set()).add(did)
+            counters = sorted({c for _, c in acc})
+            lines.append(f"### counters, mean per dispatch ({os.path.basename(f)})\n")
+            lines.append("| kernel | dispatches | " + " | ".join(counters) + " |")
+            lines.append("|---|---:|" + "---:|" * len(counters))
+            for k in sorted(disp):
+                vals = []
+                for c in counters:
+                    v = acc.get((k, c))
+                    vals.append("" if not v else "{:.6g}".format(sum(v.values()) / len(v)))
+                lines.append(f"| {k} | {len(disp[k])} | " + " | ".join(vals) + " |")
+            lines.append("")
+    print("\n".join(lines))
+
+
+def copy_probe(mib):
+    """One device copy of ``mib`` MiB through the library's copy kernel:
+    reads and writes exactly mib MiB, the scale for FETCH_SIZE/WRITE_SIZE."""
+    import ctypes
+    import torch
+    from paper_2608_28941_amd import _abi
+    rows = 1 << 17                      # 1 MiB of float64 per column
+    src = torch.ones(rows * mib, dtype=torch.float64, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    lib = _abi.load()
+    s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    _abi.check(lib.rrf_copy_matrix(_abi.RRF_F64,
+                                   ctypes.c_void_p(src.data_ptr()), rows,
+                                   ctypes.c_void_p(dst.data_ptr()), rows, rows, mib, s),
+               "rrf_copy_matrix")
+    torch.cuda.synchronize()
+    ok = bool(torch.equal(src, dst))
+    print(json.dumps({"copy_probe_mib": mib, "bytes_read": rows * mib * 8,
+                      "bytes_written": rows * mib * 8, "equal": ok}))
+    if not ok:
+        sys.exit(1)
 
 
 def algorithmic_flops(m, n, k, b):
@@ -87,11 +178,16 @@ def cpu_baseline(A_host, w, budget_cols=1024, kmax=None):
 
 def main():
     a = parse()
+    if a.summarize:
+        summarize(a.summarize)
+        return
     if a.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {a.gpus});"
               " the sharded design is described in DESIGN.md", file=sys.stderr)
         sys.exit(2)
-    import numpy as np
+    if a.copy_probe > 0:
+        copy_probe(a.copy_probe)
+        return
     import torch
     import paper_2608_28941_amd as rrf
     import workloads as W

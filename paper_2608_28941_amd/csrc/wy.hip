@@ -31,12 +31,30 @@ namespace {
 // ---------------------------------------------------------------------------
 // reduce: Z_s[c * BP + p] = sum_{r in split s} V[r, p] X[r, c]
 // grid (ceil(n / 64), nsplit), 256 threads.
+//
+// An MFMA operand puts the summation index (rows of X) on the 4 lane groups
+// and 16 columns on the lanes of a group, so a scalar load of X touches 16
+// columns with 4 rows (32 B for f64) each.  With VEC > 1 every lane loads VEC
+// consecutive rows in one 16-byte load (64 B per column per instruction) and
+// feeds them to VEC MFMA steps; the K order is permuted accordingly (row
+// offset 4 VEC u + VEC g + h for load u, lane group g, element h), and the
+// staged V rows are read in the same order.  VEC > 1 needs X, ldx and mr
+// aligned to VEC elements (the host checks).
 // ---------------------------------------------------------------------------
-template <typename T, int BP>
+template <typename T, int VEC>
+struct alignas(sizeof(T) * VEC) XPack {
+  T v[VEC];
+};
+
+template <typename T, int BP, int VEC>
 __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs<T> a) {
   typedef typename Mfma<T>::acc_t acc_t;
+  typedef XPack<T, VEC> pack_t;
   constexpr int NPT = BP / 16;
   constexpr int LDV = kRedChunk + 1;
+  constexpr int GR = 4 * VEC;              // rows of one load per column
+  constexpr int NX = kRedChunk / GR;       // loads per lane per chunk
+  static_assert(kRedChunk % GR == 0, "chunk must hold whole loads");
   __shared__ T vl[BP * LDV];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -52,18 +70,19 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs<T> a) {
 #pragma unroll
   for (int pt = 0; pt < NPT; ++pt) acc[pt] = Mfma<T>::zero();
 
-  // Loads are unconditional from clamped in-bounds addresses; rows past
-  // r_end are cancelled by zero V rows (mask multiply, so the compiler
-  // cannot turn the loads into branches), columns past n are not stored.
-  // The next chunk's X values are loaded while the current chunk computes.
-  const int64_t rlast = a.mr - 1;
-  constexpr int NX = kRedChunk / 4;   // X values per lane per chunk
-  T xcur[NX], xnxt[NX];
+  // Loads are unconditional from clamped in-bounds addresses (the last whole
+  // pack of the column); rows past r_end are cancelled by zero V rows (mask
+  // multiply, so the compiler cannot turn the loads into branches), columns
+  // past n are not stored.  The next chunk's X packs are loaded while the
+  // current chunk computes.
+  const int64_t xlast = a.mr - VEC;
+  pack_t xcur[NX], xnxt[NX];
 #pragma unroll
   for (int u = 0; u < NX; ++u) {
-    const int64_t r = r_begin + (u / 4) * 16 + 4 * (u % 4) + g;
-    xcur[u] = Xc[r < a.mr ? r : rlast];
+    const int64_t r = r_begin + GR * u + VEC * g;
+    xcur[u] = *reinterpret_cast<const pack_t*>(Xc + (r < xlast ? r : xlast));
   }
+  const int64_t rlast = a.mr - 1;
   for (int64_t R = r_begin; R < r_end; R += kRedChunk) {
     __syncthreads();
     {
@@ -81,8 +100,8 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs<T> a) {
       if (R + kRedChunk < r_end) {
 #pragma unroll
         for (int u = 0; u < NX; ++u) {
-          const int64_t rx = R + kRedChunk + (u / 4) * 16 + 4 * (u % 4) + g;
-          xnxt[u] = Xc[rx < a.mr ? rx : rlast];
+          const int64_t rx = R + kRedChunk + GR * u + VEC * g;
+          xnxt[u] = *reinterpret_cast<const pack_t*>(Xc + (rx < xlast ? rx : xlast));
         }
       }
 #pragma unroll
@@ -90,13 +109,14 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs<T> a) {
     }
     __syncthreads();
 #pragma unroll
-    for (int sl = 0; sl < kRedChunk / 16; ++sl) {
+    for (int u = 0; u < NX; ++u) {
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const T xa = xcur[sl * 4 + s];
+      for (int h = 0; h < VEC; ++h) {
+        const T xa = xcur[u].v[h];
+        const int k = GR * u + VEC * g + h;
 #pragma unroll
         for (int pt = 0; pt < NPT; ++pt) {
-          const T bv = vl[(pt * 16 + m16) * LDV + sl * 16 + 4 * s + g];
+          const T bv = vl[(pt * 16 + m16) * LDV + k];
           acc[pt] = Mfma<T>::op(xa, bv, acc[pt]);
         }
       }
@@ -344,17 +364,30 @@ hipError_t launch_update(const UpdateArgs<T>& a, int nsplit, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+template <typename T, int BP>
+hipError_t red_go(const ReduceArgs<T>& a, dim3 grid, hipStream_t s) {
+  // 16-byte packs of X when the region is aligned to them.
+  constexpr int VEC = 16 / (int)sizeof(T);
+  const bool vec_ok = (reinterpret_cast<uintptr_t>(a.X) % 16) == 0 &&
+                      a.ldx % VEC == 0 && a.mr % VEC == 0 &&
+                      a.rows_per_split % VEC == 0;
+  if (vec_ok)
+    hipLaunchKernelGGL((reduce_kernel<T, BP, VEC>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((reduce_kernel<T, BP, 1>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 template <typename T>
 hipError_t launch_reduce(const ReduceArgs<T>& a, int nsplit, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   dim3 grid((unsigned)ceil_div(a.n, kRedCols), (unsigned)nsplit);
   switch (a.bp) {
-    case 16: hipLaunchKernelGGL((reduce_kernel<T, 16>), grid, dim3(256), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((reduce_kernel<T, 32>), grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((reduce_kernel<T, 64>), grid, dim3(256), 0, s, a); break;
-    default: return hipErrorInvalidValue;
+    case 16: return red_go<T, 16>(a, grid, s);
+    case 32: return red_go<T, 32>(a, grid, s);
+    case 64: return red_go<T, 64>(a, grid, s);
   }
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
 template <typename T>
