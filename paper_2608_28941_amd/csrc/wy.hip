@@ -175,16 +175,64 @@ __global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
 }
 
 // ---------------------------------------------------------------------------
-// update: X <- X - V W (BP > 0), optional store, norms, and P = X_new Omega.
+// Buffer access to the B tiles.  A raw buffer resource (base, byte count)
+// makes the hardware bounds-check every access: an out-of-range load returns
+// zero and an out-of-range store is dropped.  Rows past mr get a lane offset
+// beyond any record count and columns past n fall beyond the record count of
+// their chunk, so the update needs no per-lane branches, its stores are
+// unconditional instructions, and the waits on the next chunk's loads never
+// have to cover the previous chunk's stores.  Offsets are 32-bit bytes: the
+// host keeps kUpdChunk * ld * sizeof(T) <= 2^30.
+// ---------------------------------------------------------------------------
+constexpr unsigned kOOB = 1u << 30;   // lane offset of a masked row
+
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, int64_t bytes) {
+  // Third word 0x00020000: the gfx9-family raw-buffer format (32-bit data).
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
+                                           (int)bytes, 0x00020000);
+}
+
+template <typename T> struct Buf;
+template <> struct Buf<double> {
+  static __device__ __forceinline__ double ld(__amdgpu_buffer_rsrc_t r, unsigned vo) {
+    return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, (int)vo, 0, 0));
+  }
+  // so: uniform byte offset (not part of the bounds check; in range here).
+  static __device__ __forceinline__ double ld_s(__amdgpu_buffer_rsrc_t r, unsigned vo, int so) {
+    return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, (int)vo, so, 0));
+  }
+  static __device__ __forceinline__ void st(double v, __amdgpu_buffer_rsrc_t r, unsigned vo) {
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, v), r, (int)vo, 0, 0);
+  }
+};
+template <> struct Buf<float> {
+  static __device__ __forceinline__ float ld(__amdgpu_buffer_rsrc_t r, unsigned vo) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)vo, 0, 0));
+  }
+  static __device__ __forceinline__ float ld_s(__amdgpu_buffer_rsrc_t r, unsigned vo, int so) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)vo, so, 0));
+  }
+  static __device__ __forceinline__ void st(float v, __amdgpu_buffer_rsrc_t r, unsigned vo) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, (int)vo, 0, 0);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// update: X <- X - V W (BP > 0), store (STORE), norms, and P = X_new Omega.
 // grid (ceil(mr / 64), nsplit), 256 threads; wavefront w owns 16 rows.
 // ---------------------------------------------------------------------------
-template <typename T, int BP, int QP>
-__global__ __launch_bounds__(256) void update_kernel(UpdateArgs<T> a) {
+template <typename T, int BP, int QP, bool STORE>
+__global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
   typedef typename Mfma<T>::acc_t acc_t;
   constexpr int NP4 = BP / 4;        // K-steps of the rank-b update
   constexpr int NQT = QP / 16;       // 16-wide tiles of the sample
   constexpr int LDW = BP + 1;        // odd: conflict-free column reads
   constexpr int LDO = QP + 1;
+  constexpr int NCT = kUpdChunk / 16;
+  constexpr int E = (int)sizeof(T);
+  static_assert(NCT == 2, "the tile schedule below assumes two tiles per chunk");
   __shared__ T wl[kUpdChunk * (BP > 0 ? LDW : 1)];
   __shared__ T ol[kUpdChunk * (QP > 0 ? LDO : 1)];
   __shared__ double nred[2][4];
@@ -196,6 +244,7 @@ __global__ __launch_bounds__(256) void update_kernel(UpdateArgs<T> a) {
   const int64_t rr = rowok ? r : 0;
   const int64_t cs = (int64_t)blockIdx.y * a.cols_per_split;
   const int64_t ce = min(a.n, cs + a.cols_per_split);
+  if (cs >= ce) return;   // uniform per workgroup, before any barrier
 
   // This wavefront's slice of -V^T as MFMA B operands: B[g][m] = -V[r][4 p4 + g].
   T vreg[NP4 > 0 ? NP4 : 1];
@@ -210,45 +259,71 @@ __global__ __launch_bounds__(256) void update_kernel(UpdateArgs<T> a) {
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) pacc[qt] = Mfma<T>::zero();
   double nb = 0.0, nt = 0.0;
-  const bool in_block = r < a.s0;
+  const double wb = r < a.s0 ? 1.0 : 0.0;   // block-row or trailing norm
+  const double wt = 1.0 - wb;
 
-  // Staging values (W, Omega) and B tiles of the next chunk are loaded into
-  // registers while the current chunk computes.  Chunks start at multiples
-  // of kUpdChunk and split boundaries are multiples of kUpdChunk, so a chunk
-  // only runs past ce at the end of the matrix, where W and Omega carry zero
-  // rows up to the next multiple; B loads use clamped in-bounds addresses
-  // (invalid rows are never stored and add nothing to the norms; invalid
-  // columns only occur past n, where the staged W and Omega rows are zero).
+  // Byte offsets.  Item i of a tile holds column drow(g, i) = drow(g, 0) +
+  // i * dstep; the lane part covers the row and drow(g, 0), the uniform part
+  // (ct * 16 + i * dstep) * ld.
+  const int d0 = Mfma<T>::drow(g, 0);
+  const int dstep = Mfma<T>::drow(0, 1) - Mfma<T>::drow(0, 0);
+  const unsigned vs = rowok ? (unsigned)((r + (int64_t)d0 * a.lds) * E) : kOOB;
+  const unsigned vd = rowok ? (unsigned)((r + (int64_t)d0 * a.ldd) * E) : kOOB;
+  const unsigned cstep_s = (unsigned)(dstep * a.lds * E);
+  const unsigned cstep_d = (unsigned)(dstep * a.ldd * E);
+  const unsigned tstep_s = (unsigned)(16 * a.lds * E);
+  const unsigned tstep_d = (unsigned)(16 * a.ldd * E);
+
+  // Staging values (W, Omega) and the B tiles of the next chunk are loaded
+  // while the current chunk computes; the last chunk prefetches itself again
+  // (harmless, and it keeps the loads unconditional).  Chunks start at
+  // multiples of kUpdChunk and split boundaries are multiples of kUpdChunk, so
+  // a chunk only runs past ce at the end of the matrix, where W and Omega
+  // carry zero rows up to the next multiple and the B loads return zero.
+  //
+  // Schedule per chunk: issue the next chunk's loads, compute and store this
+  // chunk, then (after a barrier) move the next chunk's staging values into
+  // LDS and its B tiles into the accumulators.  The waits for those loads sit
+  // in straight-line code after the stores, so they never wait for stores
+  // (the vector-memory counter retires in issue order).
   constexpr int NW = BP > 0 ? (kUpdChunk * BP) / 256 : 0;
   constexpr int NO = (kUpdChunk * QP) / 256;
-  constexpr int NCT = kUpdChunk / 16;
   static_assert((kUpdChunk * BP) % 256 == 0 && (kUpdChunk * QP) % 256 == 0,
                 "chunk staging assumes whole passes of 256 threads");
+  // W and Omega staging offsets: thread t, pass it reads row t / BP + it *
+  // (256 / BP), entry t % BP of the chunk; the pass part is uniform.
+  const unsigned wo_lane = BP > 0 ? (unsigned)(((threadIdx.x / (BP > 0 ? BP : 1)) * a.ldw +
+                                                threadIdx.x % (BP > 0 ? BP : 1)) * E) : 0u;
+  const unsigned oo_lane = QP > 0 ? (unsigned)(((threadIdx.x / (QP > 0 ? QP : 1)) * a.ldo +
+                                                threadIdx.x % (QP > 0 ? QP : 1)) * E) : 0u;
+  const int wo_pass = BP > 0 ? (256 / (BP > 0 ? BP : 1)) * a.ldw * E : 0;
+  const int oo_pass = QP > 0 ? (256 / (QP > 0 ? QP : 1)) * a.ldo * E : 0;
   T tw[NW > 0 ? NW : 1], to[NO > 0 ? NO : 1];
-  T bx[NCT][4];
+  acc_t bx[NCT];
+  const int64_t c_last = cs + (ce - cs - 1) / kUpdChunk * kUpdChunk;
   auto load_chunk = [&](int64_t cc0) {
+    if (NW > 0) {
+      const __amdgpu_buffer_rsrc_t rw =
+          buf_rsrc(a.W + cc0 * a.ldw, (int64_t)kUpdChunk * a.ldw * E);
 #pragma unroll
-    for (int it = 0; it < NW; ++it) {
-      const int idx = threadIdx.x + 256 * it;
-      tw[it] = a.W[(cc0 + idx / BP) * a.ldw + idx % BP];
+      for (int it = 0; it < NW; ++it) tw[it] = Buf<T>::ld_s(rw, wo_lane, it * wo_pass);
     }
+    if (NO > 0) {
+      const __amdgpu_buffer_rsrc_t ro =
+          buf_rsrc(a.Om + cc0 * a.ldo, (int64_t)kUpdChunk * a.ldo * E);
 #pragma unroll
-    for (int it = 0; it < NO; ++it) {
-      const int idx = threadIdx.x + 256 * it;
-      to[it] = a.Om[(cc0 + idx / QP) * a.ldo + idx % QP];
+      for (int it = 0; it < NO; ++it) to[it] = Buf<T>::ld_s(ro, oo_lane, it * oo_pass);
     }
+    const int64_t cn = min((int64_t)kUpdChunk, a.n - cc0);
+    const __amdgpu_buffer_rsrc_t rs =
+        buf_rsrc(a.src + cc0 * a.lds, ((cn - 1) * a.lds + a.mr) * E);
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t c = cc0 + ct * 16 + Mfma<T>::drow(g, i);
-        bx[ct][i] = a.src[rr + (c < a.n ? c : a.n - 1) * a.lds];
-      }
+      for (int i = 0; i < 4; ++i)
+        bx[ct][i] = Buf<T>::ld(rs, vs + ct * tstep_s + i * cstep_s);
   };
-  if (cs < ce) load_chunk(cs);
-
-  for (int64_t c0 = cs; c0 < ce; c0 += kUpdChunk) {
-    __syncthreads();
+  auto stage_chunk = [&]() {
 #pragma unroll
     for (int it = 0; it < NW; ++it) {
       const int idx = threadIdx.x + 256 * it;
@@ -259,50 +334,61 @@ __global__ __launch_bounds__(256) void update_kernel(UpdateArgs<T> a) {
       const int idx = threadIdx.x + 256 * it;
       ol[(idx / QP) * LDO + idx % QP] = to[it];
     }
-    __syncthreads();
-    T bcur[NCT][4];
+  };
+
+  acc_t t[NCT];
+  load_chunk(cs);
+  stage_chunk();
+#pragma unroll
+  for (int ct = 0; ct < NCT; ++ct) t[ct] = bx[ct];
+  __syncthreads();
+
+  for (int64_t c0 = cs; c0 < ce; c0 += kUpdChunk) {
+    load_chunk(min(c0 + kUpdChunk, c_last));
+
+    // Rank-b update of both tiles first, so that the sample of tile 0 does
+    // not wait on the result of the MFMA chain that just produced it.
+    // D[M = column drow(g, i)][N = row m16] of each 16 x 16 tile.
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) bcur[ct][i] = bx[ct][i];
-    if (c0 + kUpdChunk < ce) load_chunk(c0 + kUpdChunk);
-#pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) {
-      // D[M = column drow(g, i)][N = row m16] of this 16 x 16 tile.
-      acc_t acc;
-      bool cok[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t c = c0 + ct * 16 + Mfma<T>::drow(g, i);
-        cok[i] = c < ce;
-        acc[i] = bcur[ct][i];
-      }
-#pragma unroll
       for (int p4 = 0; p4 < NP4; ++p4) {
         const T wa = wl[(ct * 16 + m16) * LDW + 4 * p4 + g];
-        acc = Mfma<T>::op(wa, vreg[p4], acc);
+        t[ct] = Mfma<T>::op(wa, vreg[p4], t[ct]);
       }
-      if (a.dst) {
+    if (STORE) {
+      const int64_t cn = min((int64_t)kUpdChunk, a.n - c0);
+      const __amdgpu_buffer_rsrc_t rd =
+          buf_rsrc(a.dst + c0 * a.ldd, ((cn - 1) * a.ldd + a.mr) * E);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int64_t c = c0 + ct * 16 + Mfma<T>::drow(g, i);
-          if (rowok && cok[i]) a.dst[rr + c * a.ldd] = acc[i];
-        }
-      }
+      for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          Buf<T>::st(t[ct][i], rd, vd + ct * tstep_d + i * cstep_d);
+    }
+    // Invalid rows and columns hold zeros here (zero loads, zero V and W).
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const double v = (rowok && cok[i]) ? (double)acc[i] : 0.0;
-        if (in_block) nb += v * v; else nt += v * v;
+        const double v = (double)t[ct][i];
+        nb = fma(v * wb, v, nb);
+        nt = fma(v * wt, v, nt);
       }
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
+    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int qt = 0; qt < NQT; ++qt) {
           const T oa = ol[(ct * 16 + Mfma<T>::drow(g, s)) * LDO + qt * 16 + m16];
-          pacc[qt] = Mfma<T>::op(oa, acc[s], pacc[qt]);
+          pacc[qt] = Mfma<T>::op(oa, t[ct][s], pacc[qt]);
         }
-      }
-    }
+    __syncthreads();
+    stage_chunk();
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) t[ct] = bx[ct];
+    __syncthreads();
   }
 
   if (QP > 0 && rowok) {
@@ -334,7 +420,10 @@ __global__ __launch_bounds__(256) void update_kernel(UpdateArgs<T> a) {
 
 template <typename T, int BP, int QP>
 hipError_t upd_go(const UpdateArgs<T>& a, dim3 grid, hipStream_t s) {
-  hipLaunchKernelGGL((update_kernel<T, BP, QP>), grid, dim3(256), 0, s, a);
+  if (a.dst)
+    hipLaunchKernelGGL((update_kernel<T, BP, QP, true>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((update_kernel<T, BP, QP, false>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -345,21 +434,6 @@ hipError_t upd_q(const UpdateArgs<T>& a, dim3 grid, hipStream_t s) {
     case 16: return upd_go<T, BP, 16>(a, grid, s);
     case 32: return upd_go<T, BP, 32>(a, grid, s);
     case 64: return upd_go<T, BP, 64>(a, grid, s);
-  }
-  return hipErrorInvalidValue;
-}
-
-}  // namespace
-
-template <typename T>
-hipError_t launch_update(const UpdateArgs<T>& a, int nsplit, hipStream_t s) {
-  if (a.mr <= 0 || a.n <= 0) return hipSuccess;
-  dim3 grid((unsigned)ceil_div(a.mr, kUpdRows), (unsigned)nsplit);
-  switch (a.bp) {
-    case 0: return upd_q<T, 0>(a, grid, s);
-    case 16: return upd_q<T, 16>(a, grid, s);
-    case 32: return upd_q<T, 32>(a, grid, s);
-    case 64: return upd_q<T, 64>(a, grid, s);
   }
   return hipErrorInvalidValue;
 }
@@ -376,6 +450,25 @@ hipError_t red_go(const ReduceArgs<T>& a, dim3 grid, hipStream_t s) {
   else
     hipLaunchKernelGGL((reduce_kernel<T, BP, 1>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
+}
+
+}  // namespace
+
+template <typename T>
+hipError_t launch_update(const UpdateArgs<T>& a, int nsplit, hipStream_t s) {
+  if (a.mr <= 0 || a.n <= 0) return hipSuccess;
+  // 32-bit buffer offsets: a chunk of columns must span at most 2^30 bytes.
+  const int64_t ld = a.dst ? std::max(a.lds, a.ldd) : a.lds;
+  if (ld < a.mr || (int64_t)kUpdChunk * ld * (int64_t)sizeof(T) > ((int64_t)1 << 30))
+    return hipErrorInvalidValue;
+  dim3 grid((unsigned)ceil_div(a.mr, kUpdRows), (unsigned)nsplit);
+  switch (a.bp) {
+    case 0: return upd_q<T, 0>(a, grid, s);
+    case 16: return upd_q<T, 16>(a, grid, s);
+    case 32: return upd_q<T, 32>(a, grid, s);
+    case 64: return upd_q<T, 64>(a, grid, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 template <typename T>
