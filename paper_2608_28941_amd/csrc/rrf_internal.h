@@ -13,8 +13,9 @@ namespace rrf {
 constexpr int kMaxBlock = 64;      // largest block size b (MFMA tiles of 16)
 constexpr int kUpdRows = 64;       // rows per update workgroup (4 waves x 16)
 constexpr int kUpdChunk = 32;      // columns per staged chunk in the update
-constexpr int kRedCols = 64;       // columns per reduce workgroup (4 waves x 16)
-constexpr int kRedChunk = 64;      // rows per staged V chunk in the reduce
+constexpr int kRedCols = 128;      // columns per reduce workgroup (4 waves x 2 x 16)
+constexpr int kRedRows = 32;       // rows per staged V chunk in the reduce
+constexpr int kRedChunk = 64;      // granularity of the reduce's row splits
 constexpr int kPanelThreads = 256;
 constexpr int kMaxPanelWGs = 1024;
 

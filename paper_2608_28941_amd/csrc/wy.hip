@@ -30,7 +30,8 @@ namespace {
 
 // ---------------------------------------------------------------------------
 // reduce: Z_s[c * BP + p] = sum_{r in split s} V[r, p] X[r, c]
-// grid (ceil(n / 64), nsplit), 256 threads.
+// grid (ceil(n / kRedCols), nsplit), 256 threads; V is staged in chunks of
+// RC rows.
 //
 // An MFMA operand puts the summation index (rows of X) on the 4 lane groups
 // and 16 columns on the lanes of a group, so a scalar load of X touches 16
@@ -46,94 +47,119 @@ struct alignas(sizeof(T) * VEC) XPack {
   T v[VEC];
 };
 
-template <typename T, int BP, int VEC>
-__global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs<T> a) {
+template <typename T, int BP, int VEC, int CT, int RC>
+__global__ __launch_bounds__(256, 2) void reduce_kernel(ReduceArgs<T> a) {
   typedef typename Mfma<T>::acc_t acc_t;
   typedef XPack<T, VEC> pack_t;
   constexpr int NPT = BP / 16;
-  constexpr int LDV = kRedChunk + 1;
+  constexpr int LDV = RC + 1;
   constexpr int GR = 4 * VEC;              // rows of one load per column
-  constexpr int NX = kRedChunk / GR;       // loads per lane per chunk
-  static_assert(kRedChunk % GR == 0, "chunk must hold whole loads");
+  constexpr int NX = RC / GR;              // loads per lane per chunk and tile
+  constexpr int PSTEP = 256 / RC;          // reflectors staged per pass
+  constexpr int NIT = (BP * RC) / 256;     // V values per thread per chunk
+  static_assert(RC % GR == 0 && kRedChunk % RC == 0 && 256 % RC == 0 &&
+                (BP * RC) % 256 == 0, "chunk shape");
+  static_assert(kRedCols == 64 * CT, "workgroup width");
   __shared__ T vl[BP * LDV];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m16 = lane & 15, g = lane >> 4;
-  const int64_t cb = (int64_t)blockIdx.x * kRedCols + 16 * wave;
-  const int64_t col = cb + m16;
-  const bool colok = col < a.n;
+  // Wavefront w owns CT adjacent 16-column tiles; every staged V value read
+  // from LDS feeds CT MFMAs.
+  const int64_t cb = (int64_t)blockIdx.x * kRedCols + 16 * CT * wave;
   const int64_t r_begin = (int64_t)blockIdx.y * a.rows_per_split;
   const int64_t r_end = min(a.mr, r_begin + a.rows_per_split);
-  const T* Xc = a.X + (colok ? col : a.n - 1) * a.ldx;
-
-  acc_t acc[NPT];
+  const T* Xc[CT];
 #pragma unroll
-  for (int pt = 0; pt < NPT; ++pt) acc[pt] = Mfma<T>::zero();
+  for (int ct = 0; ct < CT; ++ct) {
+    const int64_t col = cb + 16 * ct + m16;
+    Xc[ct] = a.X + (col < a.n ? col : a.n - 1) * a.ldx;
+  }
+
+  acc_t acc[CT][NPT];
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int pt = 0; pt < NPT; ++pt) acc[ct][pt] = Mfma<T>::zero();
 
   // Loads are unconditional from clamped in-bounds addresses (the last whole
   // pack of the column); rows past r_end are cancelled by zero V rows (mask
   // multiply, so the compiler cannot turn the loads into branches), columns
-  // past n are not stored.  The next chunk's X packs are loaded while the
-  // current chunk computes.
+  // past n are not stored.  The next chunk's X packs and V rows are loaded
+  // into registers while the current chunk computes; after a barrier the V
+  // rows go to LDS.  Those waits sit after the compute in straight-line code.
+  // The last chunk prefetches itself again (harmless, keeps loads
+  // unconditional).
   const int64_t xlast = a.mr - VEC;
-  pack_t xcur[NX], xnxt[NX];
-#pragma unroll
-  for (int u = 0; u < NX; ++u) {
-    const int64_t r = r_begin + GR * u + VEC * g;
-    xcur[u] = *reinterpret_cast<const pack_t*>(Xc + (r < xlast ? r : xlast));
-  }
   const int64_t rlast = a.mr - 1;
-  for (int64_t R = r_begin; R < r_end; R += kRedChunk) {
-    __syncthreads();
-    {
-      // V rows of this chunk: all loads, then the next chunk's X loads, then
-      // the LDS writes (which wait for the V loads only).
-      constexpr int NIT = (BP * kRedChunk) / 256;
-      const int rr = threadIdx.x % kRedChunk;
-      const int p0 = threadIdx.x / kRedChunk;
-      const int64_t r = R + rr;
-      const double mask = r < r_end ? 1.0 : 0.0;
-      const double* Vr = a.V + (r < r_end ? r : rlast);
-      double tmp[NIT];
+  const int64_t R_last = r_begin + (r_end - r_begin - 1) / RC * RC;
+  const int rr = threadIdx.x % RC;
+  const int p0 = threadIdx.x / RC;
+  pack_t xcur[CT][NX], xnxt[CT][NX];
+  double vt[NIT];
+  auto load_x = [&](int64_t R, pack_t (*xd)[NX]) {
 #pragma unroll
-      for (int it = 0; it < NIT; ++it) tmp[it] = Vr[(int64_t)(p0 + 4 * it) * a.ldv];
-      if (R + kRedChunk < r_end) {
+    for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-        for (int u = 0; u < NX; ++u) {
-          const int64_t rx = R + kRedChunk + GR * u + VEC * g;
-          xnxt[u] = *reinterpret_cast<const pack_t*>(Xc + (rx < xlast ? rx : xlast));
-        }
+      for (int u = 0; u < NX; ++u) {
+        const int64_t r = R + GR * u + VEC * g;
+        xd[ct][u] = *reinterpret_cast<const pack_t*>(Xc[ct] + (r < xlast ? r : xlast));
       }
+  };
+  auto load_v = [&](int64_t R) {
+    const int64_t r = R + rr;
+    const double* Vr = a.V + (r < r_end ? r : rlast);
 #pragma unroll
-      for (int it = 0; it < NIT; ++it) vl[(p0 + 4 * it) * LDV + rr] = (T)(mask * tmp[it]);
-    }
-    __syncthreads();
+    for (int it = 0; it < NIT; ++it) vt[it] = Vr[(int64_t)(p0 + PSTEP * it) * a.ldv];
+  };
+  auto stage_v = [&](int64_t R) {
+    const double mask = R + rr < r_end ? 1.0 : 0.0;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) vl[(p0 + PSTEP * it) * LDV + rr] = (T)(mask * vt[it]);
+  };
+
+  load_x(r_begin, xcur);
+  load_v(r_begin);
+  stage_v(r_begin);
+  __syncthreads();
+  for (int64_t R = r_begin; R < r_end; R += RC) {
+    const int64_t Rn = min(R + RC, R_last);
+    load_x(Rn, xnxt);
+    load_v(Rn);
 #pragma unroll
     for (int u = 0; u < NX; ++u) {
 #pragma unroll
       for (int h = 0; h < VEC; ++h) {
-        const T xa = xcur[u].v[h];
         const int k = GR * u + VEC * g + h;
 #pragma unroll
         for (int pt = 0; pt < NPT; ++pt) {
           const T bv = vl[(pt * 16 + m16) * LDV + k];
-          acc[pt] = Mfma<T>::op(xa, bv, acc[pt]);
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct)
+            acc[ct][pt] = Mfma<T>::op(xcur[ct][u].v[h], bv, acc[ct][pt]);
         }
       }
     }
+    __syncthreads();
+    stage_v(Rn);
 #pragma unroll
-    for (int u = 0; u < NX; ++u) xcur[u] = xnxt[u];
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int u = 0; u < NX; ++u) xcur[ct][u] = xnxt[ct][u];
+    __syncthreads();
   }
-  // Lane holds Z^T[c = cb + drow(g, i)][p = pt * 16 + m16].
+  // Lane holds Z^T[c = cb + 16 ct + drow(g, i)][p = pt * 16 + m16].
   T* Z = a.Z + (int64_t)blockIdx.y * a.split_stride;
 #pragma unroll
-  for (int pt = 0; pt < NPT; ++pt) {
+  for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t c = cb + Mfma<T>::drow(g, i);
-      if (c < a.n) Z[c * BP + pt * 16 + m16] = acc[pt][i];
+    for (int pt = 0; pt < NPT; ++pt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t c = cb + 16 * ct + Mfma<T>::drow(g, i);
+        if (c < a.n) Z[c * BP + pt * 16 + m16] = acc[ct][pt][i];
+      }
     }
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -239,12 +265,19 @@ __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m16 = lane & 15, g = lane >> 4;
-  const int64_t r = (int64_t)blockIdx.x * kUpdRows + 16 * wave + m16;
+  const unsigned nrb = gridDim.x, rb = blockIdx.x, split = blockIdx.y;
+  const int64_t r = (int64_t)rb * kUpdRows + 16 * wave + m16;
   const bool rowok = r < a.mr;
   const int64_t rr = rowok ? r : 0;
-  const int64_t cs = (int64_t)blockIdx.y * a.cols_per_split;
+  const int64_t cs = (int64_t)split * a.cols_per_split;
   const int64_t ce = min(a.n, cs + a.cols_per_split);
-  if (cs >= ce) return;   // uniform per workgroup, before any barrier
+  if (cs >= ce) {          // empty split (uniform per workgroup, before any barrier)
+    if (a.normpart && threadIdx.x == 0) {
+      a.normpart[2 * ((int64_t)split * nrb + rb) + 0] = 0.0;
+      a.normpart[2 * ((int64_t)split * nrb + rb) + 1] = 0.0;
+    }
+    return;
+  }
 
   // This wavefront's slice of -V^T as MFMA B operands: B[g][m] = -V[r][4 p4 + g].
   T vreg[NP4 > 0 ? NP4 : 1];
@@ -392,7 +425,7 @@ __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
   }
 
   if (QP > 0 && rowok) {
-    T* P = a.P + (int64_t)blockIdx.y * a.split_stride;
+    T* P = a.P + (int64_t)split * a.split_stride;
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt)
 #pragma unroll
@@ -411,7 +444,7 @@ __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-      const int64_t wg = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+      const int64_t wg = (int64_t)split * nrb + rb;
       a.normpart[2 * wg + 0] = ((nred[0][0] + nred[0][1]) + nred[0][2]) + nred[0][3];
       a.normpart[2 * wg + 1] = ((nred[1][0] + nred[1][1]) + nred[1][2]) + nred[1][3];
     }
@@ -445,10 +478,11 @@ hipError_t red_go(const ReduceArgs<T>& a, dim3 grid, hipStream_t s) {
   const bool vec_ok = (reinterpret_cast<uintptr_t>(a.X) % 16) == 0 &&
                       a.ldx % VEC == 0 && a.mr % VEC == 0 &&
                       a.rows_per_split % VEC == 0;
+  constexpr int CT = kRedCols / 64;
   if (vec_ok)
-    hipLaunchKernelGGL((reduce_kernel<T, BP, VEC>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((reduce_kernel<T, BP, VEC, CT, kRedRows>), grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((reduce_kernel<T, BP, 1>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((reduce_kernel<T, BP, 1, CT, kRedRows>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
