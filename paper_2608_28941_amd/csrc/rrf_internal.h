@@ -11,8 +11,9 @@ namespace rrf {
 
 // Tiling constants (see each kernel for its use).
 constexpr int kMaxBlock = 64;      // largest block size b (MFMA tiles of 16)
-constexpr int kUpdRows = 64;       // rows per update workgroup (4 waves x 16)
-constexpr int kUpdChunk = 32;      // columns per staged chunk in the update
+constexpr int kUpdRowTiles = 2;    // 16-row tiles per update wavefront
+constexpr int kUpdRows = 128;      // rows per update workgroup (4 waves x 2 x 16)
+constexpr int kUpdChunk = 16;      // columns per staged chunk in the update
 constexpr int kRedCols = 128;      // columns per reduce workgroup (4 waves x 2 x 16)
 constexpr int kRedRows = 32;       // rows per staged V chunk in the reduce
 constexpr int kRedChunk = 64;      // granularity of the reduce's row splits

@@ -247,18 +247,21 @@ template <> struct Buf<float> {
 
 // ---------------------------------------------------------------------------
 // update: X <- X - V W (BP > 0), store (STORE), norms, and P = X_new Omega.
-// grid (ceil(mr / 64), nsplit), 256 threads; wavefront w owns 16 rows.
+// grid (ceil(mr / kUpdRows), nsplit), 256 threads; wavefront w owns RT
+// adjacent 16-row tiles, so every staged W and Omega value read from LDS
+// feeds RT MFMAs.
 // ---------------------------------------------------------------------------
 template <typename T, int BP, int QP, bool STORE>
 __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
   typedef typename Mfma<T>::acc_t acc_t;
+  constexpr int RT = kUpdRowTiles;
   constexpr int NP4 = BP / 4;        // K-steps of the rank-b update
   constexpr int NQT = QP / 16;       // 16-wide tiles of the sample
   constexpr int LDW = BP + 1;        // odd: conflict-free column reads
   constexpr int LDO = QP + 1;
   constexpr int NCT = kUpdChunk / 16;
   constexpr int E = (int)sizeof(T);
-  static_assert(NCT == 2, "the tile schedule below assumes two tiles per chunk");
+  static_assert(kUpdRows == 64 * RT, "workgroup height");
   __shared__ T wl[kUpdChunk * (BP > 0 ? LDW : 1)];
   __shared__ T ol[kUpdChunk * (QP > 0 ? LDO : 1)];
   __shared__ double nred[2][4];
@@ -266,9 +269,6 @@ __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m16 = lane & 15, g = lane >> 4;
   const unsigned nrb = gridDim.x, rb = blockIdx.x, split = blockIdx.y;
-  const int64_t r = (int64_t)rb * kUpdRows + 16 * wave + m16;
-  const bool rowok = r < a.mr;
-  const int64_t rr = rowok ? r : 0;
   const int64_t cs = (int64_t)split * a.cols_per_split;
   const int64_t ce = min(a.n, cs + a.cols_per_split);
   if (cs >= ce) {          // empty split (uniform per workgroup, before any barrier)
@@ -278,30 +278,50 @@ __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
     }
     return;
   }
-
-  // This wavefront's slice of -V^T as MFMA B operands: B[g][m] = -V[r][4 p4 + g].
-  T vreg[NP4 > 0 ? NP4 : 1];
-  {
-    const double vmask = rowok ? -1.0 : 0.0;   // mask multiply keeps the loads batched
+  int64_t r[RT];
+  bool rowok[RT];
 #pragma unroll
-    for (int p4 = 0; p4 < NP4; ++p4)
-      vreg[p4] = (T)(vmask * a.V[rr + (4 * p4 + g) * a.ldv]);
+  for (int rt = 0; rt < RT; ++rt) {
+    r[rt] = (int64_t)rb * kUpdRows + 16 * (RT * wave + rt) + m16;
+    rowok[rt] = r[rt] < a.mr;
   }
 
-  acc_t pacc[NQT > 0 ? NQT : 1];
+  // This wavefront's slices of -V^T as MFMA B operands:
+  // B[g][m] = -V[r[rt]][4 p4 + g].
+  T vreg[RT][NP4 > 0 ? NP4 : 1];
 #pragma unroll
-  for (int qt = 0; qt < NQT; ++qt) pacc[qt] = Mfma<T>::zero();
+  for (int rt = 0; rt < RT; ++rt) {
+    const double vmask = rowok[rt] ? -1.0 : 0.0;   // mask multiply keeps loads batched
+    const int64_t rr = rowok[rt] ? r[rt] : 0;
+#pragma unroll
+    for (int p4 = 0; p4 < NP4; ++p4)
+      vreg[rt][p4] = (T)(vmask * a.V[rr + (4 * p4 + g) * a.ldv]);
+  }
+
+  acc_t pacc[RT][NQT > 0 ? NQT : 1];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) pacc[rt][qt] = Mfma<T>::zero();
   double nb = 0.0, nt = 0.0;
-  const double wb = r < a.s0 ? 1.0 : 0.0;   // block-row or trailing norm
-  const double wt = 1.0 - wb;
+  double wb[RT], wt[RT];   // block-row or trailing norm
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    wb[rt] = r[rt] < a.s0 ? 1.0 : 0.0;
+    wt[rt] = 1.0 - wb[rt];
+  }
 
   // Byte offsets.  Item i of a tile holds column drow(g, i) = drow(g, 0) +
   // i * dstep; the lane part covers the row and drow(g, 0), the uniform part
   // (ct * 16 + i * dstep) * ld.
   const int d0 = Mfma<T>::drow(g, 0);
   const int dstep = Mfma<T>::drow(0, 1) - Mfma<T>::drow(0, 0);
-  const unsigned vs = rowok ? (unsigned)((r + (int64_t)d0 * a.lds) * E) : kOOB;
-  const unsigned vd = rowok ? (unsigned)((r + (int64_t)d0 * a.ldd) * E) : kOOB;
+  unsigned vs[RT], vd[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    vs[rt] = rowok[rt] ? (unsigned)((r[rt] + (int64_t)d0 * a.lds) * E) : kOOB;
+    vd[rt] = rowok[rt] ? (unsigned)((r[rt] + (int64_t)d0 * a.ldd) * E) : kOOB;
+  }
   const unsigned cstep_s = (unsigned)(dstep * a.lds * E);
   const unsigned cstep_d = (unsigned)(dstep * a.ldd * E);
   const unsigned tstep_s = (unsigned)(16 * a.lds * E);
@@ -332,7 +352,7 @@ __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
   const int wo_pass = BP > 0 ? (256 / (BP > 0 ? BP : 1)) * a.ldw * E : 0;
   const int oo_pass = QP > 0 ? (256 / (QP > 0 ? QP : 1)) * a.ldo * E : 0;
   T tw[NW > 0 ? NW : 1], to[NO > 0 ? NO : 1];
-  acc_t bx[NCT];
+  acc_t bx[RT][NCT];
   const int64_t c_last = cs + (ce - cs - 1) / kUpdChunk * kUpdChunk;
   auto load_chunk = [&](int64_t cc0) {
     if (NW > 0) {
@@ -351,10 +371,12 @@ __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
     const __amdgpu_buffer_rsrc_t rs =
         buf_rsrc(a.src + cc0 * a.lds, ((cn - 1) * a.lds + a.mr) * E);
 #pragma unroll
-    for (int ct = 0; ct < NCT; ++ct)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        bx[ct][i] = Buf<T>::ld(rs, vs + ct * tstep_s + i * cstep_s);
+      for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          bx[rt][ct][i] = Buf<T>::ld(rs, vs[rt] + ct * tstep_s + i * cstep_s);
   };
   auto stage_chunk = [&]() {
 #pragma unroll
@@ -369,45 +391,53 @@ __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
     }
   };
 
-  acc_t t[NCT];
+  acc_t t[RT][NCT];
   load_chunk(cs);
   stage_chunk();
 #pragma unroll
-  for (int ct = 0; ct < NCT; ++ct) t[ct] = bx[ct];
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) t[rt][ct] = bx[rt][ct];
   __syncthreads();
 
   for (int64_t c0 = cs; c0 < ce; c0 += kUpdChunk) {
     load_chunk(min(c0 + kUpdChunk, c_last));
 
-    // Rank-b update of both tiles first, so that the sample of tile 0 does
-    // not wait on the result of the MFMA chain that just produced it.
+    // Rank-b update of all tiles first, so that the samples do not wait on
+    // the result of the MFMA chain that just produced their operand.
     // D[M = column drow(g, i)][N = row m16] of each 16 x 16 tile.
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
       for (int p4 = 0; p4 < NP4; ++p4) {
         const T wa = wl[(ct * 16 + m16) * LDW + 4 * p4 + g];
-        t[ct] = Mfma<T>::op(wa, vreg[p4], t[ct]);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+          t[rt][ct] = Mfma<T>::op(wa, vreg[rt][p4], t[rt][ct]);
       }
     if (STORE) {
       const int64_t cn = min((int64_t)kUpdChunk, a.n - c0);
       const __amdgpu_buffer_rsrc_t rd =
           buf_rsrc(a.dst + c0 * a.ldd, ((cn - 1) * a.ldd + a.mr) * E);
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct)
+      for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          Buf<T>::st(t[ct][i], rd, vd + ct * tstep_d + i * cstep_d);
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            Buf<T>::st(t[rt][ct][i], rd, vd[rt] + ct * tstep_d + i * cstep_d);
     }
     // Invalid rows and columns hold zeros here (zero loads, zero V and W).
 #pragma unroll
-    for (int ct = 0; ct < NCT; ++ct)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const double v = (double)t[ct][i];
-        nb = fma(v * wb, v, nb);
-        nt = fma(v * wt, v, nt);
-      }
+      for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const double v = (double)t[rt][ct][i];
+          nb = fma(v * wb[rt], v, nb);
+          nt = fma(v * wt[rt], v, nt);
+        }
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
@@ -415,22 +445,30 @@ __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
 #pragma unroll
         for (int qt = 0; qt < NQT; ++qt) {
           const T oa = ol[(ct * 16 + Mfma<T>::drow(g, s)) * LDO + qt * 16 + m16];
-          pacc[qt] = Mfma<T>::op(oa, t[ct][s], pacc[qt]);
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt)
+            pacc[rt][qt] = Mfma<T>::op(oa, t[rt][ct][s], pacc[rt][qt]);
         }
     __syncthreads();
     stage_chunk();
 #pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) t[ct] = bx[ct];
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) t[rt][ct] = bx[rt][ct];
     __syncthreads();
   }
 
-  if (QP > 0 && rowok) {
+  if (QP > 0) {
     T* P = a.P + (int64_t)split * a.split_stride;
 #pragma unroll
-    for (int qt = 0; qt < NQT; ++qt)
+    for (int rt = 0; rt < RT; ++rt)
+      if (rowok[rt]) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        P[r + (qt * 16 + Mfma<T>::drow(g, i)) * a.ldp] = pacc[qt][i];
+        for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            P[r[rt] + (qt * 16 + Mfma<T>::drow(g, i)) * a.ldp] = pacc[rt][qt][i];
+      }
   }
   if (a.normpart) {
 #pragma unroll
