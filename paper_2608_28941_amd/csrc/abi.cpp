@@ -40,10 +40,10 @@ struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
-      rowj, bar, st, trace;
+      rowj, st, trace;
   size_t total() const {
     return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
-           normpart + red + rowj + bar + st + trace;
+           normpart + red + rowj + st + trace;
   }
 };
 
@@ -71,9 +71,9 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.Q = (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * e;
   z.Q64 = dt == RRF_F32 ? (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * 8 : 0;
   z.normpart = (size_t)(ceil_div(m_max, kUpdRows) * kMaxUpdSplits + 1) * 2 * 8;
-  z.red = (size_t)2 * kMaxPanelWGs * 64 * 8;
-  z.rowj = (size_t)2 * 64 * 8;
-  z.bar = (size_t)2 * kMaxPanelWGs * sizeof(unsigned);
+  // Panel partials: two epoch-tagged 64-bit words per value.
+  z.red = (size_t)2 * kMaxPanelWGs * 64 * 2 * 8;
+  z.rowj = (size_t)2 * 64 * 2 * 8;
   z.st = sizeof(DevState);
   z.trace = (size_t)2 * std::max<int64_t>(z.kcap, 1) * 8;
   return z;
@@ -91,12 +91,12 @@ struct rrf_plan {
   std::vector<void*> dev_allocs;
   void *Bws, *Ypart, *Om, *Zpart, *W, *Q, *Q64;
   double *V, *Tm, *tau, *Ysum;
-  double *normpart, *red, *rowj, *trace_trail_d, *trace_sub_d;
-  unsigned* bar;
+  double *normpart, *trace_trail_d, *trace_sub_d;
+  unsigned long long *red, *rowj;
   DevState* st;
   DevState* st_host;
   int stop_mode, timing, panel_target;
-  unsigned panel_launches;   // epochs of the panel's publication flags
+  unsigned panel_launches;   // epochs of the panel's tagged partials
   // last run
   int64_t last_m, last_n, last_k, last_b, nblocks;
   double E0, sigma2;
@@ -197,7 +197,7 @@ void stats_collect(rrf_plan* p) {
   } while (0)
 
 // Epoch base of the next panel launch: a nonzero multiple of 128 (the
-// flags are zeroed at plan creation and a step adds j + 1 <= 64).
+// tagged partials are zeroed at plan creation and a step adds j + 1 <= 64).
 unsigned next_epoch(rrf_plan* p) {
   p->panel_launches = (p->panel_launches + 1u) & 0x1FFFFFFu;
   if (p->panel_launches == 0u) p->panel_launches = 1u;
@@ -318,7 +318,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     pa.m = mp; pa.b = (int)bi;
     pa.V = V + k + k * ldb; pa.ldv = ldb;
     pa.Tm = Tm + k * kTLd; pa.ldt = kTLd; pa.tau = tau + k;
-    pa.red = p->red; pa.rowj = p->rowj; pa.flags = p->bar; pa.st = p->st; pa.G = sh.G;
+    pa.red = p->red; pa.rowj = p->rowj; pa.st = p->st; pa.G = sh.G;
     pa.epoch_base = next_epoch(p);
     RRF_LAUNCH(p, RRF_STAGE_PANEL,
                2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi,
@@ -456,7 +456,7 @@ rrf_status panel_stage(rrf_plan* p, const T* Y, int64_t m, int64_t b,
   pa.m = m; pa.b = (int)b;
   pa.V = p->V; pa.ldv = p->sz.ldb;
   pa.Tm = p->Tm; pa.ldt = kTLd; pa.tau = p->tau;
-  pa.red = p->red; pa.rowj = p->rowj; pa.flags = p->bar; pa.st = p->st; pa.G = sh.G;
+  pa.red = p->red; pa.rowj = p->rowj; pa.st = p->st; pa.G = sh.G;
   pa.epoch_base = next_epoch(p);
   hipError_t e = launch_panel(pa, sh, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->V, p->sz.ldb, Vout, ldv, m, b, s);
@@ -576,7 +576,6 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   RRF_ALLOC(normpart, p->sz.normpart);
   RRF_ALLOC(red, p->sz.red);
   RRF_ALLOC(rowj, p->sz.rowj);
-  RRF_ALLOC(bar, p->sz.bar);
   RRF_ALLOC(st, p->sz.st);
   RRF_ALLOC(trace_trail_d, p->sz.trace / 2);
   RRF_ALLOC(trace_sub_d, p->sz.trace / 2);
@@ -587,7 +586,8 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
     if (f && std::atoi(f) == counter) e = hipErrorOutOfMemory;
     else e = hipHostMalloc((void**)&p->st_host, sizeof(DevState), 0);
   }
-  if (e == hipSuccess) e = hipMemsetAsync(p->bar, 0, p->sz.bar, p->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(p->red, 0, p->sz.red, p->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(p->rowj, 0, p->sz.rowj, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->st, 0, p->sz.st, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->Om, 0, p->sz.Om, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->V, 0, p->sz.V, p->stream);
@@ -650,10 +650,6 @@ rrf_status rrf_run(rrf_plan_t plan, const void* A, int64_t m, int64_t n,
                            &kk, &warn);
     if (st != RRF_OK) {
       (void)hipStreamSynchronize(plan->stream);
-      if (plan->st_host && plan->st_host->barrier_err) {
-        (void)launch_zero_u32(plan->bar, 2 * kMaxPanelWGs, plan->stream);
-        (void)hipStreamSynchronize(plan->stream);
-      }
       plan->nblocks = 0;
       *k = 0;
       return st;

@@ -83,11 +83,6 @@ __global__ void convert_kernel(const Ts* src, int64_t lds, Td* dst, int64_t ldd,
     dst[r + c * ldd] = (Td)src[r + c * lds];
 }
 
-__global__ void zero_u32_kernel(unsigned* p, int count) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < count) p[i] = 0u;
-}
-
 }  // namespace
 
 hipError_t launch_finalize(const double* normpart, int nparts, DevState* st,
@@ -126,13 +121,6 @@ hipError_t launch_convert(const Ts* src, int64_t lds, Td* dst, int64_t ldd,
   dim3 grid((unsigned)ceil_div(rows, 256), (unsigned)(cols < 4096 ? cols : 4096));
   hipLaunchKernelGGL((convert_kernel<Ts, Td>), grid, dim3(256), 0, s, src, lds,
                      dst, ldd, rows, cols);
-  return hipGetLastError();
-}
-
-hipError_t launch_zero_u32(unsigned* p, int count, hipStream_t s) {
-  if (count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_u32_kernel, dim3((count + 255) / 256), dim3(256), 0,
-                     s, p, count);
   return hipGetLastError();
 }
 

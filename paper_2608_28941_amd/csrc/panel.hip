@@ -39,57 +39,51 @@ constexpr unsigned kSpinLimit = 1u << 24;
 // across the XCDs without L2 write-back or invalidation, which an
 // agent-scope fence would cost on every step).
 //
-// Publication: wave 0 of workgroup w stores its partials with agent-scope
-// relaxed stores, waits until they have completed (s_waitcnt vmcnt(0)), then
-// stores flags[par][w] = epoch.  A reader waits, one lane per flag, until
-// every flag of the step carries the step's epoch, then reads the partials
-// with agent-scope loads issued after the wait.  Epochs are unique per launch
-// and step, so flags left by earlier launches never match.  The wait is
-// bounded: after kSpinLimit polls it records an error and every later wait
-// returns at once, so the kernel always drains.
-__device__ __forceinline__ void st_agent(double* p, double v) {
-  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p),
-                     (unsigned long long)__double_as_longlong(v),
-                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Publication without flags: a workgroup publishes each double of its step
+// partials as two 64-bit words, each holding one 32-bit half of the value in
+// its upper half and the step's epoch in its lower half.  A 64-bit atomic
+// access is single-copy atomic, so a reader that sees the step's epoch in
+// both words of a value has that step's value; it re-reads until every word
+// it needs carries the epoch.  One trip through the coherent memory path per
+// step instead of three (partials, completion wait, flag, flag poll, partial
+// read).  Epochs are unique per launch and step (the buffer is zeroed at
+// plan creation and epoch 0 is never used), so words left by earlier steps
+// or launches never match.  A slot is rewritten two steps later only by a
+// workgroup that has seen every workgroup's next-step partials, so no reader
+// is still reading it.  The wait is bounded: after kSpinLimit polls it
+// records an error and every later wait returns at once, so the kernel
+// always drains (the results are then discarded by the host).
+typedef unsigned long long u64;
+
+__device__ __forceinline__ void put_tagged(u64* p, double v, unsigned epoch) {
+  const u64 u = (u64)__double_as_longlong(v);
+  __hip_atomic_store(p, (u & 0xFFFFFFFF00000000ull) | epoch, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(p + 1, (u << 32) | epoch, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ double ld_agent(const double* p) {
-  const unsigned long long u = __hip_atomic_load(
-      reinterpret_cast<const unsigned long long*>(p), __ATOMIC_RELAXED,
-      __HIP_MEMORY_SCOPE_AGENT);
-  return __longlong_as_double((long long)u);
+__device__ __forceinline__ u64 get_word(const u64* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double untag(u64 hi, u64 lo) {
+  return __longlong_as_double((long long)((hi & 0xFFFFFFFF00000000ull) | (lo >> 32)));
+}
+__device__ __forceinline__ bool tagged(u64 w, unsigned epoch) {
+  return (unsigned)w == epoch;
 }
 
-// s_waitcnt vmcnt(0) with expcnt and lgkmcnt left at their maxima (gfx9
-// encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[15:14]).
-constexpr unsigned kWaitVmcnt0 = 0x0F70;
-
-__device__ __forceinline__ void publish(unsigned* flag, unsigned epoch) {
-  if (threadIdx.x < 64) {
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    if (threadIdx.x == 0)
-      __hip_atomic_store(flag, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// One poll round failed: back off, count, and give up (recording the error)
+// after kSpinLimit rounds or once another thread has given up.
+__device__ __forceinline__ bool keep_waiting(unsigned* spins, DevState* st) {
+  __builtin_amdgcn_s_sleep(2);
+  ++*spins;
+  if ((*spins & 255u) == 0u &&
+      (*spins > kSpinLimit ||
+       __hip_atomic_load(&st->barrier_err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)) {
+    __hip_atomic_store(&st->barrier_err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return false;
   }
-}
-
-__device__ __forceinline__ void wait_all(const unsigned* flags, int G,
-                                         unsigned epoch, DevState* st) {
-  if ((int)threadIdx.x < G) {
-    unsigned spins = 0;
-    while (__hip_atomic_load(&flags[threadIdx.x], __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT) != epoch) {
-      __builtin_amdgcn_s_sleep(1);
-      ++spins;
-      if ((spins & 255u) == 0u &&
-          (spins > kSpinLimit ||
-           __hip_atomic_load(&st->barrier_err, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT) != 0)) {
-        __hip_atomic_store(&st->barrier_err, 1, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-        break;
-      }
-    }
-  }
-  __syncthreads();
+  return true;
 }
 
 template <int BP, int RPT>
@@ -99,7 +93,8 @@ __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs a) {
   static_assert(RW >= BP, "rows 0..b-1 must sit in workgroup 0");
   __shared__ double xs[RW];
   __shared__ double rowj_s[BP];
-  __shared__ double red_l[GR][BP];
+  __shared__ double red_l[GR][BP];   // step partials of this workgroup
+  __shared__ double red_r[GR][BP];   // sums of the gathered partials
   __shared__ double tot[BP], rj[BP];
   __shared__ double Tl[BP][BP + 1];
   __shared__ double Ej[BP];          // v_p^T v_j, p < j, of the last step
@@ -163,44 +158,61 @@ __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs a) {
     for (int q = 0; q < RPT; ++q) d += col[q] * xs[g + GR * q];
     red_l[g][k] = d;
     __syncthreads();
-    // 3. Workgroup partial to global memory (wave 0), then publish.  While
+    // 3. Workgroup partial to global memory as epoch-tagged words.  While
     //    the other workgroups catch up, workgroup 0 finishes the previous
     //    column of T.
     const unsigned epoch = a.epoch_base + (unsigned)j + 1u;
     if (t < BP) {
       double s = 0.0;
       for (int gg = 0; gg < GR; ++gg) s += red_l[gg][t];
-      st_agent(&a.red[((int64_t)par * a.G + w) * BP + t], s);
-      if (w == 0) st_agent(&a.rowj[par * BP + t], rowj_s[t]);
+      put_tagged(&a.red[(((int64_t)par * a.G + w) * BP + t) * 2], s, epoch);
+      if (w == 0) put_tagged(&a.rowj[(par * BP + t) * 2], rowj_s[t], epoch);
     }
-    publish(&a.flags[par * kMaxPanelWGs + w], epoch);
     if (w == 0 && j > 0) t_column(j - 1);
-    wait_all(a.flags + par * kMaxPanelWGs, a.G, epoch, a.st);
-    // 4. Every workgroup sums all partials in the same fixed order; row j is
-    //    loaded in the same batch.
+    // 4. Every workgroup sums all partials in the same fixed order, polling
+    //    each batch until it is complete; row j is read the same way.
     {
       const int kk = t % BP, sub = t / BP;
-      const double* rp = a.red + (int64_t)par * a.G * BP + kk;
-      const double rjv = (t < BP) ? ld_agent(&a.rowj[par * BP + t]) : 0.0;
+      const u64* rp = a.red + ((int64_t)par * a.G * BP + kk) * 2;
+      unsigned spins = 0;
+      if (t < BP) {
+        const u64* q = &a.rowj[(par * BP + t) * 2];
+        u64 hi = get_word(q), lo = get_word(q + 1);
+        while (!(tagged(hi, epoch) && tagged(lo, epoch)) && keep_waiting(&spins, a.st)) {
+          hi = get_word(q);
+          lo = get_word(q + 1);
+        }
+        rj[t] = untag(hi, lo);
+      }
       double s = 0.0;
       for (int w0 = sub; w0 < a.G; w0 += 16 * GR) {
-        double v[16];
+        u64 hi[16], lo[16];
+        bool ok;
+        do {
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const int ww = w0 + u * GR;
-          v[u] = ld_agent(&rp[(int64_t)(ww < a.G ? ww : 0) * BP]);
-        }
+          for (int u = 0; u < 16; ++u) {
+            const int ww = w0 + u * GR;
+            const u64* q = &rp[(int64_t)(ww < a.G ? ww : 0) * BP * 2];
+            hi[u] = get_word(q);
+            lo[u] = get_word(q + 1);
+          }
+          ok = true;
+#pragma unroll
+          for (int u = 0; u < 16; ++u)
+            ok = ok && tagged(hi[u], epoch) && tagged(lo[u], epoch);
+        } while (!ok && keep_waiting(&spins, a.st));
 #pragma unroll
         for (int u = 0; u < 16; ++u)
-          if (w0 + u * GR < a.G) s += v[u];
+          if (w0 + u * GR < a.G) s += untag(hi[u], lo[u]);
       }
-      red_l[sub][kk] = s;
-      if (t < BP) rj[t] = rjv;
+      // red_r, not red_l: threads of other wavefronts may still be
+      // reading red_l in step 3.
+      red_r[sub][kk] = s;
     }
     __syncthreads();
     if (t < BP) {
       double s = 0.0;
-      for (int gg = 0; gg < GR; ++gg) s += red_l[gg][t];
+      for (int gg = 0; gg < GR; ++gg) s += red_r[gg][t];
       tot[t] = s;
     }
     __syncthreads();

@@ -80,9 +80,8 @@ struct PanelArgs {
   double* V; int64_t ldv;      // m x BP output (binary64 for both dtypes)
   double* Tm; int64_t ldt;     // BP x BP output
   double* tau;                 // b outputs
-  double* red;                 // 2 x G x BP
-  double* rowj;                // 2 x BP
-  unsigned* flags;             // 2 x kMaxPanelWGs publication flags
+  unsigned long long* red;     // 2 x G x BP epoch-tagged values (2 words each)
+  unsigned long long* rowj;    // 2 x BP epoch-tagged values
   unsigned epoch_base;         // unique per launch, multiple of 128, > 0
   DevState* st;
   int G;
@@ -128,6 +127,5 @@ hipError_t launch_copy(const T* src, int64_t lds, T* dst, int64_t ldd,
 template <typename Ts, typename Td>
 hipError_t launch_convert(const Ts* src, int64_t lds, Td* dst, int64_t ldd,
                           int64_t rows, int64_t cols, hipStream_t s);
-hipError_t launch_zero_u32(unsigned* p, int count, hipStream_t s);
 
 }  // namespace rrf
