@@ -40,10 +40,10 @@ struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
-      rowj, st, trace;
+      rowj, st, trace, Zpart2, W2;
   size_t total() const {
     return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
-           normpart + red + rowj + st + trace;
+           normpart + red + rowj + st + trace + Zpart2 + W2;
   }
 };
 
@@ -76,6 +76,9 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.rowj = (size_t)2 * 64 * 2 * 8;
   z.st = sizeof(DevState);
   z.trace = (size_t)2 * std::max<int64_t>(z.kcap, 1) * 8;
+  // Look-ahead: Q_i^T applied to the m x b sample (64 columns at most).
+  z.Zpart2 = (size_t)kMaxRedSplits * 64 * 64 * 8;
+  z.W2 = (size_t)(64 + kUpdChunk) * 64 * 8;
   return z;
 }
 
@@ -86,10 +89,12 @@ struct rrf_plan {
   size_t elem;
   int64_t m_max, n_max, b_max, k_max;
   hipStream_t stream;
+  int lookahead;             // factor the next panel during the update
   int device, num_cus;
   Sizes sz;
   std::vector<void*> dev_allocs;
   void *Bws, *Ypart, *Om, *Zpart, *W, *Q, *Q64;
+  double *Zpart2, *W2;       // scratch of the look-ahead's small reflector application
   double *V, *Tm, *tau, *Ysum;
   double *normpart, *trace_trail_d, *trace_sub_d;
   unsigned long long *red, *rowj;
@@ -162,7 +167,7 @@ void stats_reset(rrf_plan* p) {
   p->event_stage.clear();
 }
 
-hipError_t ev_mark(rrf_plan* p, int stage) {
+hipError_t ev_mark(rrf_plan* p, int stage, hipStream_t s) {
   if (!p->timing) return hipSuccess;
   if (p->events_used == p->events.size()) {
     hipEvent_t e;
@@ -172,7 +177,7 @@ hipError_t ev_mark(rrf_plan* p, int stage) {
   }
   if (p->event_stage.size() < p->events_used + 1) p->event_stage.resize(p->events_used + 1);
   p->event_stage[p->events_used] = stage;
-  return hipEventRecord(p->events[p->events_used++], p->stream);
+  return hipEventRecord(p->events[p->events_used++], s);
 }
 
 // Pairs of events (begin, end) were recorded per launch.
@@ -185,16 +190,19 @@ void stats_collect(rrf_plan* p) {
   }
 }
 
-#define RRF_LAUNCH(p, stage, fl, by, expr)                 \
+// Launch on stream s_ with per-launch statistics (and HIP-event timing when
+// enabled: a begin/end pair on the launch's own stream).
+#define RRF_LAUNCH_ON(p, s_, stage, fl, by, expr)          \
   do {                                                     \
-    hipError_t e_ = ev_mark((p), (stage));                 \
+    hipError_t e_ = ev_mark((p), (stage), (s_));           \
     if (e_ == hipSuccess) e_ = (expr);                     \
-    if (e_ == hipSuccess) e_ = ev_mark((p), (stage));      \
+    if (e_ == hipSuccess) e_ = ev_mark((p), (stage), (s_)); \
     if (e_ != hipSuccess) return hip_fail(e_);             \
     (p)->launches[stage] += 1;                             \
     (p)->flops[stage] += (fl);                             \
     (p)->bytes[stage] += (by);                             \
   } while (0)
+#define RRF_LAUNCH(p, stage, fl, by, expr) RRF_LAUNCH_ON(p, (p)->stream, stage, fl, by, expr)
 
 // Epoch base of the next panel launch: a nonzero multiple of 128 (the
 // tagged partials are zeroed at plan creation and a step adds j + 1 <= 64).
@@ -216,22 +224,25 @@ hipError_t read_state(rrf_plan* p) {
 template <typename T>
 rrf_status apply_wy(rrf_plan* p, int trans, const double* V, int64_t ldv,
                     const double* Tm, int64_t ldt, int b, int bp, T* X,
-                    int64_t ldx, int64_t mr, int64_t ncols, int stage) {
+                    int64_t ldx, int64_t mr, int64_t ncols, int stage,
+                    T* Zs = nullptr, T* Ws = nullptr) {
   if (mr <= 0 || ncols <= 0) return RRF_OK;
+  if (!Zs) Zs = (T*)p->Zpart;
+  if (!Ws) Ws = (T*)p->W;
   const double e = (double)sizeof(T);
   const int sr0 = red_splits(mr, ncols, p->num_cus);
   ReduceArgs<T> ra{};
   ra.X = X; ra.ldx = ldx; ra.mr = mr; ra.n = ncols;
   ra.V = V; ra.ldv = ldv; ra.bp = bp;
-  ra.Z = (T*)p->Zpart; ra.split_stride = ncols * bp;
+  ra.Z = Zs; ra.split_stride = ncols * bp;
   ra.rows_per_split = round_up(ceil_div(mr, sr0), kRedChunk);
   const int sr = (int)ceil_div(mr, ra.rows_per_split);
   const double fl = 2.0 * mr * ncols * b;
   RRF_LAUNCH(p, stage == RRF_STAGE_UPDATE ? RRF_STAGE_REDUCE : stage, fl,
              e * mr * ncols, launch_reduce<T>(ra, sr, p->stream));
   FormWArgs<T> fa{};
-  fa.Z = (T*)p->Zpart; fa.nsplit = sr; fa.split_stride = ra.split_stride;
-  fa.Tm = Tm; fa.ldt = ldt; fa.W = (T*)p->W; fa.n = ncols; fa.bp = bp;
+  fa.Z = Zs; fa.nsplit = sr; fa.split_stride = ra.split_stride;
+  fa.Tm = Tm; fa.ldt = ldt; fa.W = Ws; fa.n = ncols; fa.bp = bp;
   fa.trans = trans;
   fa.b = b;
   RRF_LAUNCH(p, stage == RRF_STAGE_UPDATE ? RRF_STAGE_FORMW : stage,
@@ -239,7 +250,7 @@ rrf_status apply_wy(rrf_plan* p, int trans, const double* V, int64_t ldv,
              launch_formw<T>(fa, p->stream));
   UpdateArgs<T> ua{};
   ua.src = X; ua.lds = ldx; ua.dst = X; ua.ldd = ldx; ua.mr = mr; ua.n = ncols;
-  ua.V = V; ua.ldv = ldv; ua.bp = bp; ua.W = (T*)p->W; ua.ldw = bp;
+  ua.V = V; ua.ldv = ldv; ua.bp = bp; ua.W = Ws; ua.ldw = bp;
   ua.Om = nullptr; ua.ldo = kOmLd; ua.qp = 0; ua.P = nullptr; ua.ldp = 0;
   ua.split_stride = 0; ua.s0 = 0; ua.normpart = nullptr;
   const int su0 = upd_splits(mr, ncols, p->num_cus);
@@ -298,34 +309,71 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   if (he != hipSuccess) return hip_fail(he);
   if (p->st_host->nonfinite) return RRF_ERR_NONFINITE;
 
+  // Look-ahead (the paper's two-queue overlap, Sec. 5, on one GPU): the
+  // update of block i samples Omega_{i+2} instead of Omega_{i+1}; the sample
+  // for block i + 1 is the one the previous update took, S_{i+1} = B^(i)
+  // Omega_{i+1}, brought up to date with the redundant panel update
+  // Y_{i+1} = Q_i^T S_{i+1} as soon as W_i exists (Q_i^T (B Omega) =
+  // (Q_i^T B) Omega).  The panel of block i + 1 is then factored by a few
+  // workgroups of the update's own launch while the rest update B.
+  // It pays when the panel grid is small: a panel of more than a quarter of
+  // the compute units takes too many slots from the update it runs beside.
+  bool la = p->lookahead != 0 && kcap > b;
+  if (la) {
+    PanelShape sh1;
+    la = panel_shape(m - b, (int)std::min(b, kcap - b), p->num_cus, p->panel_target, &sh1) &&
+         sh1.G <= p->num_cus / 4;
+  }
   int64_t k = 0;
-  int64_t yoff = 0;
+  int64_t yoff = 0;          // row offset of the next sample in the slabs
   int blk = 0;
+  bool panel_ready = false;  // the panel of this block was factored by the last update
   bool stop = p->st_host->stop != 0;
   while (!stop) {
     const int64_t bi = std::min(b, kcap - k);
     const int bp = pad16(bi);
     const int64_t mp = m - k;
     p->block_start.push_back(k);
-    PanelShape sh;
-    if (!panel_shape(mp, (int)bi, p->num_cus, p->panel_target, &sh)) return RRF_ERR_SHAPE;
-    RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mp * bi * ysplits + 8.0 * mp * bi,
-               launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
-                                      (int)bi, bp, sh.rows_pad, p->Ysum,
-                                      p->sz.ldysum, s));
-    PanelArgs pa{};
-    pa.Y = p->Ysum; pa.ldy = p->sz.ldysum;
-    pa.m = mp; pa.b = (int)bi;
-    pa.V = V + k + k * ldb; pa.ldv = ldb;
-    pa.Tm = Tm + k * kTLd; pa.ldt = kTLd; pa.tau = tau + k;
-    pa.red = p->red; pa.rowj = p->rowj; pa.st = p->st; pa.G = sh.G;
-    pa.epoch_base = next_epoch(p);
-    RRF_LAUNCH(p, RRF_STAGE_PANEL,
-               2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi,
-               16.0 * mp * bi, launch_panel(pa, sh, s));
+    if (panel_ready) {
+      panel_ready = false;
+    } else {
+      PanelShape sh;
+      if (!panel_shape(mp, (int)bi, p->num_cus, p->panel_target, &sh)) return RRF_ERR_SHAPE;
+      RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mp * bi * ysplits + 8.0 * mp * bi,
+                 launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
+                                        (int)bi, bp, sh.rows_pad, p->Ysum,
+                                        p->sz.ldysum, s));
+      PanelArgs pa{};
+      pa.Y = p->Ysum; pa.ldy = p->sz.ldysum;
+      pa.m = mp; pa.b = (int)bi;
+      pa.V = V + k + k * ldb; pa.ldv = ldb;
+      pa.Tm = Tm + k * kTLd; pa.ldt = kTLd; pa.tau = tau + k;
+      pa.red = p->red; pa.rowj = p->rowj; pa.st = p->st; pa.G = sh.G;
+      pa.epoch_base = next_epoch(p);
+      RRF_LAUNCH(p, RRF_STAGE_PANEL,
+                 2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi,
+                 16.0 * mp * bi, launch_panel(pa, sh, s));
+    }
 
+    const int64_t k_next = k + bi;
+    const int64_t b_next = k_next < kcap ? std::min(b, kcap - k_next) : 0;
     const T* src = blk == 0 ? A : Bws;
     const int64_t lsrc = blk == 0 ? lda : ldb;
+
+    // Look-ahead, block 0: S_1 = A Omega_1 (later blocks get their look-ahead
+    // sample from the previous update).
+    if (la && blk == 0 && b_next > 0) {
+      RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
+                 launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_next, b_next,
+                                  Om, kOmLd, 1, s));
+      UpdateArgs<T> u1 = u;
+      u1.qp = pad16(b_next);
+      u1.normpart = nullptr;
+      RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 2.0 * m * n * b_next, e * (m * n + m * b_next),
+                 launch_update<T>(u1, ysplits, s));
+      yoff = 0;
+    }
+
     // Z = V_i^T B[k:m, :], W = T_i^T Z.
     const int sr0 = red_splits(mp, n, p->num_cus);
     ReduceArgs<T> ra{};
@@ -344,28 +392,75 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     RRF_LAUNCH(p, RRF_STAGE_FORMW, 1.0 * n * bi * bi, e * n * bi * (sr + 1),
                launch_formw<T>(fa, s));
 
-    // Next sketch block (speculative: the stop test comes after the update).
-    const int64_t k_next = k + bi;
-    const int64_t b_next = k_next < kcap ? std::min(b, kcap - k_next) : 0;
-    const int q_next = b_next > 0 ? pad16(b_next) : 0;
-    if (b_next > 0)
-      RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
-                 launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_next,
-                                  b_next, Om, kOmLd, 1, s));
+    PanelArgs pan{};          // look-ahead panel of block i + 1
+    PanelShape pan_shape{};
+    double pan_flops = 0.0, pan_bytes = 0.0;
+    if (la && b_next > 0) {
+      // Y_{i+1} = Q_i^T S_{i+1}[rows k..m), in binary64; its panel (rows
+      // k_next..m) is factored with the update below.
+      const int64_t mpn = mp - bi;
+      const int bpn = pad16(b_next);
+      PanelShape shn;
+      if (!panel_shape(mpn, (int)b_next, p->num_cus, p->panel_target, &shn))
+        return RRF_ERR_SHAPE;
+      RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mp * b_next * ysplits + 8.0 * mp * b_next,
+                 launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
+                                        (int)b_next, bpn, bi + shn.rows_pad,
+                                        p->Ysum, p->sz.ldysum, s));
+      rrf_status rs = apply_wy<double>(p, 1, V + k + k * ldb, ldb, Tm + k * kTLd,
+                                       kTLd, (int)bi, bp, p->Ysum, p->sz.ldysum,
+                                       mp, b_next, RRF_STAGE_PANEL, p->Zpart2, p->W2);
+      if (rs != RRF_OK) return rs;
+      pan.Y = p->Ysum + bi; pan.ldy = p->sz.ldysum;
+      pan.m = mpn; pan.b = (int)b_next;
+      pan.V = V + k_next + k_next * ldb; pan.ldv = ldb;
+      pan.Tm = Tm + k_next * kTLd; pan.ldt = kTLd; pan.tau = tau + k_next;
+      pan.red = p->red; pan.rowj = p->rowj; pan.st = p->st; pan.G = shn.G;
+      pan_shape = shn;
+      pan_flops = 2.0 * mpn * b_next * b_next - 2.0 / 3.0 * b_next * b_next * b_next +
+                  1.0 * mpn * b_next * b_next;
+      pan_bytes = 16.0 * mpn * b_next;
+      panel_ready = true;
+    }
 
-    // B[k:m, :] -= V_i W, fused with the next sample and the norms.
+    // Sketch block sampled by this update (speculative: the stop test comes
+    // after the update): Omega_{i+1}, or Omega_{i+2} with look-ahead.
+    const int64_t k_s = la ? k_next + b_next : k_next;
+    const int64_t b_s = (la ? (b_next > 0 && k_s < kcap) : b_next > 0)
+                            ? std::min(b, kcap - k_s) : 0;
+    const int q_s = b_s > 0 ? pad16(b_s) : 0;
+    if (b_s > 0)
+      RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_s,
+                 launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_s, b_s, Om,
+                                  kOmLd, 1, s));
+
+    // B[k:m, :] -= V_i W, fused with the sample and the norms.
     UpdateArgs<T> ua{};
     ua.src = src + k; ua.lds = lsrc; ua.dst = Bws + k; ua.ldd = ldb;
     ua.mr = mp; ua.n = n; ua.V = V + k + k * ldb; ua.ldv = ldb; ua.bp = bp;
-    ua.W = (T*)p->W; ua.ldw = bp; ua.Om = Om; ua.ldo = kOmLd; ua.qp = q_next;
+    ua.W = (T*)p->W; ua.ldw = bp; ua.Om = Om; ua.ldo = kOmLd; ua.qp = q_s;
     ua.P = Yp; ua.ldp = ldb; ua.split_stride = ldb * 64; ua.s0 = bi;
     ua.normpart = p->normpart;
     const int su0 = upd_splits(mp, n, p->num_cus);
     ua.cols_per_split = round_up(ceil_div(n, su0), kUpdChunk);
     const int su = (int)ceil_div(n, ua.cols_per_split);
-    RRF_LAUNCH(p, RRF_STAGE_UPDATE,
-               2.0 * mp * n * bi + 2.0 * (mp - bi) * n * b_next,
-               2.0 * e * mp * n, launch_update<T>(ua, su, s));
+    const double upd_flops = 2.0 * mp * n * bi + 2.0 * (mp - bi) * n * b_s;
+    if (panel_ready) {
+      pan.epoch_base = next_epoch(p);
+      if (update_panel_supported(bp, q_s, pan_shape)) {
+        RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops + pan_flops,
+                   2.0 * e * mp * n + pan_bytes,
+                   launch_update_panel<T>(ua, su, pan, pan_shape, s));
+      } else {
+        RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops, 2.0 * e * mp * n,
+                   launch_update<T>(ua, su, s));
+        RRF_LAUNCH(p, RRF_STAGE_PANEL, pan_flops, pan_bytes,
+                   launch_panel(pan, pan_shape, s));
+      }
+    } else {
+      RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops, 2.0 * e * mp * n,
+                 launch_update<T>(ua, su, s));
+    }
     nparts = (int)(ceil_div(mp, kUpdRows) * su);
     RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
                launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
@@ -538,6 +633,10 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
     const int v = std::atoi(pt);
     if (v >= 1 && v <= kMaxPanelWGs) p->panel_target = v;
   }
+  // RRF_LOOKAHEAD=0 factors every panel after the update that samples it (no
+  // overlap); the default factors the next panel during the update.
+  p->lookahead = 1;
+  if (const char* la = std::getenv("RRF_LOOKAHEAD")) p->lookahead = std::atoi(la) != 0;
   if (hipGetDevice(&p->device) != hipSuccess ||
       hipDeviceGetAttribute(&p->num_cus, hipDeviceAttributeMultiprocessorCount,
                             p->device) != hipSuccess) {
@@ -574,6 +673,8 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   RRF_ALLOC(Q, p->sz.Q);
   if (p->sz.Q64) RRF_ALLOC(Q64, p->sz.Q64);
   RRF_ALLOC(normpart, p->sz.normpart);
+  RRF_ALLOC(Zpart2, p->sz.Zpart2);
+  RRF_ALLOC(W2, p->sz.W2);
   RRF_ALLOC(red, p->sz.red);
   RRF_ALLOC(rowj, p->sz.rowj);
   RRF_ALLOC(st, p->sz.st);

@@ -1,269 +1,15 @@
-// Panel Householder QR with T factor (Alg. 2, geqrt step).
-//
-// Factors the sampled panel Y (m x b, b <= 64) column by column with LAPACK
-// dlarfg / geqr2 semantics and builds the compact WY factor T (Eq. (4)) on the
-// fly by the forward columnwise recursion T[:j, j] = -tau_j T[:j, :j] V^T v_j.
-//
-// Layout: a cooperative grid of G workgroups of 256 threads.  Thread t owns
-// column k = t % BP and row group g = t / BP; workgroup w owns rows
-// [w RW, (w + 1) RW) with RW = (256 / BP) * RPT, and thread (k, g) keeps the
-// RPT rows w RW + g + (256 / BP) q of column k in registers for the whole
-// factorisation.  Column j is broadcast through LDS.
-//
-// One grid-wide reduction per column.  With x the current column j below the
-// diagonal, every thread contributes the partial dot of its own column with x
-// over rows > j; together with row j of every column (held by workgroup 0)
-// this gives, in one reduction,
-//   ||x||^2            (the dlarfg norm),
-//   v_j^T y_k, k > j   (the rank-1 update of the trailing columns), and
-//   v_k^T v_j, k < j   (the new column of T),
-// because v_j = [1; x / (alpha - beta)].  Every workgroup sums the partials
-// in the same order, so all derive identical scalars (deterministic, no
-// floating-point atomics).
-//
-// The panel is gathered beforehand into a zero-padded binary64 buffer (the
-// sum of the update's column-split partials); the factorisation runs in
-// binary64 (registers, reductions, V, T, tau), so the reflectors are
-// orthogonal to binary64 precision even for float data.
-//
-// Requires 256 / BP * RPT >= BP so that rows 0 .. b-1 sit in workgroup 0.
+// Panel Householder QR with T factor (Alg. 2, geqrt step): the cooperative
+// panel kernel (its workgroup body is in panel_body.h), the gather of the
+// sampled panel and the launchers.
 
-#include "rrf_internal.h"
+#include "panel_body.h"
 
 namespace rrf {
 namespace {
 
-constexpr unsigned kSpinLimit = 1u << 24;
-
-// Cross-workgroup traffic uses agent-scope atomic accesses only (coherent
-// across the XCDs without L2 write-back or invalidation, which an
-// agent-scope fence would cost on every step).
-//
-// Publication without flags: a workgroup publishes each double of its step
-// partials as two 64-bit words, each holding one 32-bit half of the value in
-// its upper half and the step's epoch in its lower half.  A 64-bit atomic
-// access is single-copy atomic, so a reader that sees the step's epoch in
-// both words of a value has that step's value; it re-reads until every word
-// it needs carries the epoch.  One trip through the coherent memory path per
-// step instead of three (partials, completion wait, flag, flag poll, partial
-// read).  Epochs are unique per launch and step (the buffer is zeroed at
-// plan creation and epoch 0 is never used), so words left by earlier steps
-// or launches never match.  A slot is rewritten two steps later only by a
-// workgroup that has seen every workgroup's next-step partials, so no reader
-// is still reading it.  The wait is bounded: after kSpinLimit polls it
-// records an error and every later wait returns at once, so the kernel
-// always drains (the results are then discarded by the host).
-typedef unsigned long long u64;
-
-__device__ __forceinline__ void put_tagged(u64* p, double v, unsigned epoch) {
-  const u64 u = (u64)__double_as_longlong(v);
-  __hip_atomic_store(p, (u & 0xFFFFFFFF00000000ull) | epoch, __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-  __hip_atomic_store(p + 1, (u << 32) | epoch, __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ u64 get_word(const u64* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ double untag(u64 hi, u64 lo) {
-  return __longlong_as_double((long long)((hi & 0xFFFFFFFF00000000ull) | (lo >> 32)));
-}
-__device__ __forceinline__ bool tagged(u64 w, unsigned epoch) {
-  return (unsigned)w == epoch;
-}
-
-// One poll round failed: back off, count, and give up (recording the error)
-// after kSpinLimit rounds or once another thread has given up.
-__device__ __forceinline__ bool keep_waiting(unsigned* spins, DevState* st) {
-  __builtin_amdgcn_s_sleep(2);
-  ++*spins;
-  if ((*spins & 255u) == 0u &&
-      (*spins > kSpinLimit ||
-       __hip_atomic_load(&st->barrier_err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)) {
-    __hip_atomic_store(&st->barrier_err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return false;
-  }
-  return true;
-}
-
 template <int BP, int RPT>
 __global__ __launch_bounds__(kPanelThreads) void panel_kernel(PanelArgs a) {
-  constexpr int GR = kPanelThreads / BP;
-  constexpr int RW = GR * RPT;
-  static_assert(RW >= BP, "rows 0..b-1 must sit in workgroup 0");
-  __shared__ double xs[RW];
-  __shared__ double rowj_s[BP];
-  __shared__ double red_l[GR][BP];   // step partials of this workgroup
-  __shared__ double red_r[GR][BP];   // sums of the gathered partials
-  __shared__ double tot[BP], rj[BP];
-  __shared__ double Tl[BP][BP + 1];
-  __shared__ double Ej[BP];          // v_p^T v_j, p < j, of the last step
-  __shared__ double tau_s[BP];
-
-  const int t = threadIdx.x;
-  const int k = t % BP, g = t / BP;
-  const int w = blockIdx.x;
-  const int64_t base = (int64_t)w * RW;
-  const int b = a.b;
-
-  // The gathered panel has G * RW rows and BP columns, zero outside (m, b),
-  // so the RPT loads are unconditional and all in flight together.
-  double col[RPT];
-  {
-    const double* Yk = a.Y + base + g + (int64_t)k * a.ldy;
-#pragma unroll
-    for (int q = 0; q < RPT; ++q) col[q] = Yk[GR * q];
-  }
-
-  // Column jj of T (workgroup 0) from Ej and tau_s: the forward columnwise
-  // recursion T[:jj, jj] = -tau_jj T[:jj, :jj] (V^T v_jj).
-  auto t_column = [&](int jj) {
-    if (t < jj) {
-      double acc = 0.0;
-      for (int p = t; p < jj; ++p) acc += Tl[t][p] * Ej[p];
-      Tl[t][jj] = -tau_s[jj] * acc;
-    } else if (t == jj) {
-      Tl[jj][jj] = tau_s[jj];
-    }
-  };
-
-  for (int j = 0; j < b; ++j) {
-    const int par = j & 1;
-    // 1. Broadcast column j with its rows <= j zeroed: then every dot below
-    //    is over rows > j and the rank-1 update leaves rows <= j untouched,
-    //    with no per-row conditions.  Row j of every column sits in
-    //    workgroup 0 (row group j % GR, register j / GR).
-    constexpr int QJ = (BP + GR - 1) / GR;   // registers that can hold rows < BP
-    if (k == j) {
-      if (w == 0) {
-#pragma unroll
-        for (int q = 0; q < RPT; ++q)
-          xs[g + GR * q] = (q < QJ && g + GR * q <= j) ? 0.0 : col[q];
-      } else {
-#pragma unroll
-        for (int q = 0; q < RPT; ++q) xs[g + GR * q] = col[q];
-      }
-    }
-    if (w == 0 && g == j % GR) {
-      const int qj = j / GR;
-      double v = 0.0;
-#pragma unroll
-      for (int q = 0; q < QJ; ++q) v = (q == qj) ? col[q] : v;
-      rowj_s[k] = v;
-    }
-    __syncthreads();
-    // 2. Partial dot of this thread's column with x (rows > j).
-    double d = 0.0;
-#pragma unroll
-    for (int q = 0; q < RPT; ++q) d += col[q] * xs[g + GR * q];
-    red_l[g][k] = d;
-    __syncthreads();
-    // 3. Workgroup partial to global memory as epoch-tagged words.  While
-    //    the other workgroups catch up, workgroup 0 finishes the previous
-    //    column of T.
-    const unsigned epoch = a.epoch_base + (unsigned)j + 1u;
-    if (t < BP) {
-      double s = 0.0;
-      for (int gg = 0; gg < GR; ++gg) s += red_l[gg][t];
-      put_tagged(&a.red[(((int64_t)par * a.G + w) * BP + t) * 2], s, epoch);
-      if (w == 0) put_tagged(&a.rowj[(par * BP + t) * 2], rowj_s[t], epoch);
-    }
-    if (w == 0 && j > 0) t_column(j - 1);
-    // 4. Every workgroup sums all partials in the same fixed order, polling
-    //    each batch until it is complete; row j is read the same way.
-    {
-      const int kk = t % BP, sub = t / BP;
-      const u64* rp = a.red + ((int64_t)par * a.G * BP + kk) * 2;
-      unsigned spins = 0;
-      if (t < BP) {
-        const u64* q = &a.rowj[(par * BP + t) * 2];
-        u64 hi = get_word(q), lo = get_word(q + 1);
-        while (!(tagged(hi, epoch) && tagged(lo, epoch)) && keep_waiting(&spins, a.st)) {
-          hi = get_word(q);
-          lo = get_word(q + 1);
-        }
-        rj[t] = untag(hi, lo);
-      }
-      double s = 0.0;
-      for (int w0 = sub; w0 < a.G; w0 += 16 * GR) {
-        u64 hi[16], lo[16];
-        bool ok;
-        do {
-#pragma unroll
-          for (int u = 0; u < 16; ++u) {
-            const int ww = w0 + u * GR;
-            const u64* q = &rp[(int64_t)(ww < a.G ? ww : 0) * BP * 2];
-            hi[u] = get_word(q);
-            lo[u] = get_word(q + 1);
-          }
-          ok = true;
-#pragma unroll
-          for (int u = 0; u < 16; ++u)
-            ok = ok && tagged(hi[u], epoch) && tagged(lo[u], epoch);
-        } while (!ok && keep_waiting(&spins, a.st));
-#pragma unroll
-        for (int u = 0; u < 16; ++u)
-          if (w0 + u * GR < a.G) s += untag(hi[u], lo[u]);
-      }
-      // red_r, not red_l: threads of other wavefronts may still be
-      // reading red_l in step 3.
-      red_r[sub][kk] = s;
-    }
-    __syncthreads();
-    if (t < BP) {
-      double s = 0.0;
-      for (int gg = 0; gg < GR; ++gg) s += red_r[gg][t];
-      tot[t] = s;
-    }
-    __syncthreads();
-    // 5. dlarfg scalars (identical in every workgroup).
-    const double alpha = rj[j];
-    const double xi2 = tot[j];
-    double tau_j = 0.0, scale = 0.0;
-    if (xi2 != 0.0) {
-      const double nrm = sqrt(alpha * alpha + xi2);
-      const double beta = (alpha >= 0.0) ? -nrm : nrm;
-      tau_j = (beta - alpha) / beta;
-      scale = 1.0 / (alpha - beta);
-    }
-    // 6. v_j = x * scale below the diagonal (rows <= j of column j are never
-    //    read again); trailing columns y_k -= tau_j (v_j^T y_k) v_j with
-    //    v_j^T y_k = y_k[j] + scale * dot_k (xs is zero on rows <= j).
-    if (k == j) {
-#pragma unroll
-      for (int q = 0; q < RPT; ++q) col[q] = col[q] * scale;
-    } else if (k > j && k < b) {
-      const double fs = tau_j * (rj[k] + scale * tot[k]) * scale;
-#pragma unroll
-      for (int q = 0; q < RPT; ++q) col[q] = col[q] - fs * xs[g + GR * q];
-    }
-    // 7. Save v_p^T v_j = V[j, p] + scale * dot_p (p < j) for T (workgroup 0).
-    if (w == 0) {
-      if (t < j) Ej[t] = rj[t] + scale * tot[t];
-      else if (t == j) tau_s[j] = tau_j;
-    }
-    __syncthreads();
-  }
-  if (w == 0 && b > 0) t_column(b - 1);
-  __syncthreads();
-
-  // Outputs: V with explicit unit diagonal and zeros above / beyond b.
-#pragma unroll
-  for (int q = 0; q < RPT; ++q) {
-    const int64_t r = base + g + GR * q;
-    if (r < a.m) {
-      double v = 0.0;
-      if (k < b) v = (r > k) ? col[q] : (r == k ? 1.0 : 0.0);
-      a.V[r + k * a.ldv] = v;
-    }
-  }
-  if (w == 0) {
-    for (int idx = t; idx < BP * BP; idx += kPanelThreads) {
-      const int i = idx % BP, jj = idx / BP;
-      a.Tm[i + (int64_t)jj * a.ldt] = (jj < b && i <= jj) ? Tl[i][jj] : 0.0;
-    }
-    if (t < b) a.tau[t] = Tl[t][t];
-  }
+  panel_body<BP, RPT>(a, (int)blockIdx.x);
 }
 
 template <typename T>

@@ -106,6 +106,13 @@ hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s);
 struct PanelShape { int bp, rpt, G; int64_t rows_pad; };
 bool panel_shape(int64_t m, int b, int num_cus, int target_wgs, PanelShape* out);
 hipError_t launch_panel(const PanelArgs& a, const PanelShape& sh, hipStream_t s);
+// Look-ahead: the update (store, sample width qp) and the panel of the next
+// block in one launch; supported when bp == qp == the panel's padded width.
+bool update_panel_supported(int bp, int qp, const PanelShape& sh);
+template <typename T>
+hipError_t launch_update_panel(const UpdateArgs<T>& ua, int nsplit,
+                               const PanelArgs& pa, const PanelShape& sh,
+                               hipStream_t s);
 // Ysum[r + k * ldy] = sum_s P_s[r + k * ldp] for r < m, k < b; 0 elsewhere
 // for r < rows_pad, k < bp (binary64).
 template <typename T>
