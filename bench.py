@@ -5,6 +5,11 @@
     python bench.py --copy-probe MIB      one plain device copy of MIB MiB
                                           (calibrates the HBM byte counters)
     python bench.py --summarize DIR...    per-kernel summary of rocprofv3 CSVs
+    python bench.py --pmc-report DIR... --copy-fetch D --copy-write D
+                    [--traffic-out FILE --kernel NAME --workload W]
+                                          counters per kernel, HBM bytes scaled
+                                          by the copy probe, and the traffic
+                                          record bench.py reads
 
 A step is one rrf_run (Alg. 2 to the tolerance, then explicit Q and B) with A
 already resident in HBM.  Prints one JSON line:
@@ -46,7 +51,129 @@ def parse():
                     help="only run one device-to-device copy of MIB MiB")
     ap.add_argument("--summarize", nargs="+", default=None, metavar="DIR",
                     help="only summarise rocprofv3 CSV output (no GPU)")
+    ap.add_argument("--pmc-report", nargs="+", default=None, metavar="DIR",
+                    help="only report rocprofv3 --pmc CSV output (no GPU)")
+    ap.add_argument("--copy-fetch", default=None, help="copy-probe FETCH_SIZE run")
+    ap.add_argument("--copy-write", default=None, help="copy-probe WRITE_SIZE run")
+    ap.add_argument("--traffic-out", default=None, help="write the traffic record here")
+    ap.add_argument("--kernel", default=None, help="kernel of the traffic record")
     return ap.parse_args()
+
+
+CSRC = os.path.join(ROOT, "paper_2608_28941_amd", "csrc")
+COPY_PROBE_KERNEL = "copy_kernel<double>"
+
+
+def sources_sha256():
+    """Hash of the HIP/C++ sources: a traffic record is valid only for them."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def read_counters(dirs):
+    """{kernel: {dispatch_id: {counter: value, "_ns": duration}}} from the
+    counter_collection CSVs under dirs (values summed over instances)."""
+    import csv
+    import glob
+    out = {}
+    for d in dirs:
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                k = short_kernel(r["Kernel_Name"])
+                disp = out.setdefault(k, {}).setdefault((f, r["Dispatch_Id"]), {})
+                c = r["Counter_Name"]
+                disp[c] = disp.get(c, 0.0) + float(r["Counter_Value"])
+                disp["_ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    return out
+
+
+def copy_scale(d, counter, known_bytes):
+    """Bytes per counted byte, from the copy probe's single copy dispatch."""
+    c = read_counters([d]).get(COPY_PROBE_KERNEL, {})
+    vals = [v[counter] for v in c.values() if counter in v]
+    if not vals:
+        raise SystemExit(f"no {COPY_PROBE_KERNEL} {counter} in {d}")
+    return known_bytes / (vals[0] * 1024.0)
+
+
+def pmc_report(a):
+    mib = 1024   # the copy probe that the calibration runs use
+    known = mib * (1 << 20)
+    fs = copy_scale(a.copy_fetch, "FETCH_SIZE", known) if a.copy_fetch else None
+    ws = copy_scale(a.copy_write, "WRITE_SIZE", known) if a.copy_write else None
+    cnt = read_counters(a.pmc_report)
+    lines = ["| kernel | dispatches | avg us (counter run) | read GB/launch | write GB/launch | "
+             "HBM GB/s | MFMA TFLOP/s | MFMA busy |", "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    rec = None
+    for k in sorted(cnt, key=lambda x: -sum(v.get("_ns", 0) for v in cnt[x].values())):
+        disp = list(cnt[k].values())
+        def mean(c):
+            v = [d[c] for d in disp if c in d]
+            return sum(v) / len(v) if v else None
+        ns = [d["_ns"] for d in disp if "FETCH_SIZE" in d or "WRITE_SIZE" in d] or \
+             [d["_ns"] for d in disp]
+        avg_ns = sum(ns) / len(ns)
+        rd = mean("FETCH_SIZE")
+        wr = mean("WRITE_SIZE")
+        rd = rd * 1024.0 * fs if (rd is not None and fs) else None
+        wr = wr * 1024.0 * ws if (wr is not None and ws) else None
+        f64 = mean("SQ_INSTS_VALU_MFMA_MOPS_F64")
+        f32 = mean("SQ_INSTS_VALU_MFMA_MOPS_F32")
+        mops = (f64 or 0.0) + (f32 or 0.0)
+        mfma_ns = [d["_ns"] for d in disp if "SQ_INSTS_VALU_MFMA_MOPS_F64" in d] or ns
+        mfma_avg_ns = sum(mfma_ns) / len(mfma_ns)
+        busy = mean("SQ_VALU_MFMA_BUSY_CYCLES")
+        gui = mean("GRBM_GUI_ACTIVE")
+        busy_frac = busy / (gui / 8.0 * 4 * 256) if (busy is not None and gui) else None
+        gbs = ((rd or 0.0) + (wr or 0.0)) / avg_ns if (rd is not None or wr is not None) else None
+        tf = mops * 512.0 / mfma_avg_ns / 1e3 if mops else None
+        def fmt(x, f):
+            return "" if x is None else f.format(x)
+        lines.append(f"| {k} | {len(disp)} | {avg_ns / 1e3:.1f} | {fmt(rd and rd / 1e9, '{:.4f}')} | "
+                     f"{fmt(wr and wr / 1e9, '{:.4f}')} | {fmt(gbs, '{:.0f}')} | {fmt(tf, '{:.2f}')} | "
+                     f"{fmt(busy_frac, '{:.1%}')} |")
+        if a.kernel and k == a.kernel:
+            rec = {"rd": rd, "wr": wr, "n": sum(1 for d in disp if "FETCH_SIZE" in d)}
+    print(f"copy-probe scale: FETCH_SIZE x{fs}, WRITE_SIZE x{ws} (bytes per counted byte)\n")
+    print("\n".join(lines))
+    if a.traffic_out:
+        if not rec or rec["rd"] is None or rec["wr"] is None:
+            raise SystemExit(f"no FETCH_SIZE/WRITE_SIZE for {a.kernel}")
+        with open(a.traffic_out, "w") as f:
+            f.write("# HBM traffic per launch of the dominant kernel: rocprofv3 --pmc FETCH_SIZE\n"
+                    "# and WRITE_SIZE (KiB per dispatch) scaled by what the same counters read for a\n"
+                    "# plain copy of known size (bench.py --copy-probe), averaged over the launches\n"
+                    "# of one run.  Valid only for the sources with the hash below.\n")
+            f.write(f"workload {a.workload}\nkernel {a.kernel}\nsources_sha256 {sources_sha256()}\n")
+            f.write(f"fetch_scale {fs:.6f}\nwrite_scale {ws:.6f}\nlaunches {rec['n']}\n")
+            f.write(f"fetch_bytes_per_launch {rec['rd']:.6e}\nwrite_bytes_per_launch {rec['wr']:.6e}\n")
+            f.write(f"traffic_bytes_per_launch {rec['rd'] + rec['wr']:.6e}\n")
+
+
+def read_traffic(workload):
+    """Bytes per launch of the dominant kernel from the committed record, or
+    None when there is none for this workload or the sources have changed."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        key, _, val = line.strip().partition(" ")
+        rec[key] = val.strip()
+    if rec.get("workload") != workload or rec.get("sources_sha256") != sources_sha256():
+        return None
+    try:
+        return float(rec["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def short_kernel(name):
@@ -181,6 +308,9 @@ def main():
     if a.summarize:
         summarize(a.summarize)
         return
+    if a.pmc_report:
+        pmc_report(a)
+        return
     if a.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {a.gpus});"
               " the sharded design is described in DESIGN.md", file=sys.stderr)
@@ -243,9 +373,14 @@ def main():
     if stages:
         upd = stages["update"]
         ach = upd["flops"] / (upd["ms"] * 1e-3) / 1e12 if upd["ms"] > 0 else 0.0
-        roof = {"bound": "mfma", "kernel": "update_kernel (B -= V W, next sample, norms)",
+        traffic = read_traffic(w.name)
+        roof = {"bound": "mfma",
+                "kernel": "update (B -= V W, next sample, norms; with look-ahead also "
+                          "the next panel)",
                 "achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(ach / peak, 4), "traffic": None,
+                "frac": round(ach / peak, 4),
+                "traffic": None if traffic is None else round(traffic, 0),
+                "traffic_unit": "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE)",
                 "avg_launch_ms": upd["ms"] / max(upd["launches"], 1),
                 "launches_per_step": upd["launches"]}
         gf = sum(stages[s]["flops"] for s in GEMM_STAGES)
