@@ -14,6 +14,9 @@ Based on an Implicit Householder QR Decomposition"):
                      Alg. 2, sketch step).
 * ``hbarrf``      -- Alg. 2 step by step, with unblocked Householder
                      reflections (geqr2 semantics), in float64.
+* ``stability``   -- the Sec. 6 stability experiment (Fig. 3) in fp32:
+                     Alg. 2 against block Gram-Schmidt (Alg. 1) with and
+                     without reorthogonalisation (``python -m oracle.stability``).
 
 Every function cites the passage it follows.  Pins against independent facts
 (LAPACK, SVD, closed forms, invariants) live in ``tests/test_oracle_*.py``.
