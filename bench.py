@@ -2,6 +2,10 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline]
+    python bench.py --fixed-rank R[,R..]  fixed-rank mode (k_max = R, tol = 0)
+                                          against a one-shot pipeline with the
+                                          same sketch (rocBLAS GEMMs, rocSOLVER
+                                          QR through torch), Sec. 6 / Fig. 6
     python bench.py --copy-probe MIB      one plain device copy of MIB MiB
                                           (calibrates the HBM byte counters)
     python bench.py --summarize DIR...    per-kernel summary of rocprofv3 CSVs
@@ -47,6 +51,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=3,
                     help="extra runs with per-kernel HIP-event timing")
+    ap.add_argument("--fixed-rank", default=None, metavar="R[,R..]",
+                    help="only the fixed-rank comparison at these ranks")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run one device-to-device copy of MIB MiB")
     ap.add_argument("--summarize", nargs="+", default=None, metavar="DIR",
@@ -236,6 +242,70 @@ def summarize(dirs):
     print("\n".join(lines))
 
 
+def fixed_rank(a):
+    """Fixed-rank mode (Sec. 6, Fig. 6): rrf_run with k_max = r and tol = 0
+    (r columns in r / b blocks, RRF_WARN_KMAX expected) against the one-shot
+    fixed-rank range finder on the same GPU and the same sketch Omega
+    (columns 0..r-1 of RRF-NORMAL-v1): Y = A Omega, Q = qr(Y) (rocSOLVER
+    geqrf + orgqr via torch), B = Q^T A.  The reference pipeline is a
+    measurement only.  Prints one JSON line."""
+    import torch
+    import paper_2608_28941_amd as rrf
+    import workloads as W
+    w = W.WORKLOADS[a.workload]
+    A_host = W.build_matrix(w)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    tdt = torch.float64 if w.dtype == "float64" else torch.float32
+    A = rrf.colmajor(torch.from_numpy(A_host).to(dev))
+    Ar = A.contiguous()                       # row-major copy for torch's GEMMs
+    normA = float(torch.linalg.norm(A.double()))
+    ranks = [int(x) for x in a.fixed_rank.split(",")]
+    out = []
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            r = fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / reps, r
+
+    for r in ranks:
+        b = min(w.block_b, 64)
+        with rrf.Plan(tdt, w.m, w.n, b, k_max=r) as plan:
+            def ours():
+                return plan.run_raw(A, 0.0, b, w.sketch_seed)
+            t_ours, res = timed(ours, a.steps)
+            k = res[2]
+            Q, B, _ = plan.run(A, 0.0, b, w.sketch_seed)
+            res_ours = float(torch.linalg.norm((A - Q @ B).double())) / normA
+        Om = rrf.sketch(tdt, w.sketch_seed, w.n, 0, r)
+
+        def oneshot():
+            Y = Ar @ Om
+            Qo, _ = torch.linalg.qr(Y)
+            Bo = Qo.t().contiguous() @ Ar
+            return Qo, Bo
+        t_ref, (Qo, Bo) = timed(oneshot, a.steps)
+        res_ref = float(torch.linalg.norm((Ar - Qo @ Bo).double())) / normA
+        fl = algorithmic_flops(w.m, w.n, k, b)
+        fl_ref = 2.0 * w.m * w.n * r + 4.0 * w.m * r * r - 4.0 / 3.0 * r ** 3 + 2.0 * w.m * w.n * r
+        out.append({"r": r, "k": k, "ours_ms": round(t_ours * 1e3, 3),
+                    "ours_gflops": round(fl / t_ours / 1e9, 1),
+                    "ours_residual": res_ours,
+                    "oneshot_ms": round(t_ref * 1e3, 3),
+                    "oneshot_gflops": round(fl_ref / t_ref / 1e9, 1),
+                    "oneshot_residual": res_ref})
+        print(f"[fixed-rank] r={r} ours {t_ours*1e3:.2f} ms one-shot {t_ref*1e3:.2f} ms",
+              file=sys.stderr, flush=True)
+        del Om, Qo, Bo
+    print(json.dumps({"metric": "fixed-rank wall time (ms), ours vs one-shot pipeline",
+                      "workload": w.name, "dtype": w.dtype, "block_b": min(w.block_b, 64),
+                      "steps": a.steps, "results": out}))
+
+
 def copy_probe(mib):
     """One device copy of ``mib`` MiB through the library's copy kernel:
     reads and writes exactly mib MiB, the scale for FETCH_SIZE/WRITE_SIZE."""
@@ -317,6 +387,9 @@ def main():
         sys.exit(2)
     if a.copy_probe > 0:
         copy_probe(a.copy_probe)
+        return
+    if a.fixed_rank:
+        fixed_rank(a)
         return
     import torch
     import paper_2608_28941_amd as rrf
