@@ -34,22 +34,23 @@ namespace {
 constexpr int kMaxUpdSplits = 8;
 constexpr int kMaxRedSplits = 32;
 constexpr int kOmLd = 64;         // Omega stored [c][q] with row length 64
+constexpr int kPanelGrid = 0;      // column-by-column panel, one grid reduction per column
+constexpr int kPanelTsqr = 1;      // tall-skinny QR + Householder reconstruction
 constexpr int kTLd = 64;          // T stored like geqrt's T: 64 rows
 
 struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
-      rowj, st, trace, Zpart2, W2;
+      rowj, st, trace, Zpart2, W2, tsqr;
   size_t total() const {
     return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
-           normpart + red + rowj + st + trace + Zpart2 + W2;
+           normpart + red + rowj + st + trace + Zpart2 + W2 + tsqr;
   }
 };
 
 Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
                     int64_t k_max) {
-  (void)b_max;
   Sizes z;
   const size_t e = dt == RRF_F32 ? 4 : 8;
   // 64 rows of slack: the reduce reads whole 64-row chunks of V.
@@ -79,6 +80,14 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   // Look-ahead: Q_i^T applied to the m x b sample (64 columns at most).
   z.Zpart2 = (size_t)kMaxRedSplits * 64 * 64 * 8;
   z.W2 = (size_t)(64 + kUpdChunk) * 64 * 8;
+  // Tall-skinny QR panel: the largest tree over the block widths the plan
+  // allows (the tree shrinks with the panel's rows).
+  z.tsqr = 8;
+  for (int bb = 16; bb <= pad16(std::max<int64_t>(b_max, 1)); bb *= 2) {
+    TsqrShape ts;
+    if (tsqr_shape(std::max<int64_t>(m_max, bb), bb, &ts))
+      z.tsqr = std::max(z.tsqr, (size_t)ts.scratch_elems * 8);
+  }
   return z;
 }
 
@@ -95,6 +104,8 @@ struct rrf_plan {
   std::vector<void*> dev_allocs;
   void *Bws, *Ypart, *Om, *Zpart, *W, *Q, *Q64;
   double *Zpart2, *W2;       // scratch of the look-ahead's small reflector application
+  double* tsqr;              // scratch of the tall-skinny QR panel
+  int panel_mode;            // kPanelGrid or kPanelTsqr
   double *V, *Tm, *tau, *Ysum;
   double *normpart, *trace_trail_d, *trace_sub_d;
   unsigned long long *red, *rowj;
@@ -219,6 +230,21 @@ hipError_t read_state(rrf_plan* p) {
   return hipStreamSynchronize(p->stream);
 }
 
+// Panel QR of the gathered panel pa.Y (m x b) into pa.V, pa.Tm, pa.tau with
+// the plan's panel algorithm (pa.Y is overwritten by the tall-skinny QR).
+bool panel_fits(rrf_plan* p, int64_t m, int b, PanelShape* sh) {
+  return panel_shape(m, b, p->num_cus, p->panel_target, sh);
+}
+hipError_t run_panel(rrf_plan* p, PanelArgs& pa, const PanelShape& sh, hipStream_t s) {
+  if (p->panel_mode == kPanelTsqr) {
+    TsqrShape ts;
+    if (!tsqr_shape(pa.m, pa.b, &ts)) return hipErrorInvalidValue;
+    return launch_panel_tsqr(pa, ts, p->tsqr, s);
+  }
+  pa.epoch_base = next_epoch(p);
+  return launch_panel(pa, sh, s);
+}
+
 // X (mr x ncols) <- (I - V T V^T)^T X (trans) or (I - V T V^T) X, with V, T
 // already zero padded to bp columns in plan-compatible layout.
 template <typename T>
@@ -318,7 +344,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   // workgroups of the update's own launch while the rest update B.
   // It pays when the panel grid is small: a panel of more than a quarter of
   // the compute units takes too many slots from the update it runs beside.
-  bool la = p->lookahead != 0 && kcap > b;
+  bool la = p->lookahead != 0 && p->panel_mode == kPanelGrid && kcap > b;
   if (la) {
     PanelShape sh1;
     la = panel_shape(m - b, (int)std::min(b, kcap - b), p->num_cus, p->panel_target, &sh1) &&
@@ -349,10 +375,9 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       pa.V = V + k + k * ldb; pa.ldv = ldb;
       pa.Tm = Tm + k * kTLd; pa.ldt = kTLd; pa.tau = tau + k;
       pa.red = p->red; pa.rowj = p->rowj; pa.st = p->st; pa.G = sh.G;
-      pa.epoch_base = next_epoch(p);
       RRF_LAUNCH(p, RRF_STAGE_PANEL,
                  2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi,
-                 16.0 * mp * bi, launch_panel(pa, sh, s));
+                 16.0 * mp * bi, run_panel(p, pa, sh, s));
     }
 
     const int64_t k_next = k + bi;
@@ -455,7 +480,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
         RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops, 2.0 * e * mp * n,
                    launch_update<T>(ua, su, s));
         RRF_LAUNCH(p, RRF_STAGE_PANEL, pan_flops, pan_bytes,
-                   launch_panel(pan, pan_shape, s));
+                   run_panel(p, pan, pan_shape, s));
       }
     } else {
       RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops, 2.0 * e * mp * n,
@@ -552,8 +577,7 @@ rrf_status panel_stage(rrf_plan* p, const T* Y, int64_t m, int64_t b,
   pa.V = p->V; pa.ldv = p->sz.ldb;
   pa.Tm = p->Tm; pa.ldt = kTLd; pa.tau = p->tau;
   pa.red = p->red; pa.rowj = p->rowj; pa.st = p->st; pa.G = sh.G;
-  pa.epoch_base = next_epoch(p);
-  hipError_t e = launch_panel(pa, sh, s);
+  hipError_t e = run_panel(p, pa, sh, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->V, p->sz.ldb, Vout, ldv, m, b, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->Tm, kTLd, Tout, ldt, b, b, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->tau, 1, tauout, 1, b, 1, s);
@@ -637,6 +661,12 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   // overlap); the default factors the next panel during the update.
   p->lookahead = 1;
   if (const char* la = std::getenv("RRF_LOOKAHEAD")) p->lookahead = std::atoi(la) != 0;
+  // RRF_PANEL=tsqr selects the tall-skinny QR panel with Householder
+  // reconstruction; the default is the column-by-column panel (one grid-wide
+  // reduction per column), the only one the look-ahead overlaps.
+  p->panel_mode = kPanelGrid;
+  if (const char* pm = std::getenv("RRF_PANEL"))
+    if (std::strcmp(pm, "tsqr") == 0) p->panel_mode = kPanelTsqr;
   if (hipGetDevice(&p->device) != hipSuccess ||
       hipDeviceGetAttribute(&p->num_cus, hipDeviceAttributeMultiprocessorCount,
                             p->device) != hipSuccess) {
@@ -674,6 +704,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   if (p->sz.Q64) RRF_ALLOC(Q64, p->sz.Q64);
   RRF_ALLOC(normpart, p->sz.normpart);
   RRF_ALLOC(Zpart2, p->sz.Zpart2);
+  RRF_ALLOC(tsqr, p->sz.tsqr);
   RRF_ALLOC(W2, p->sz.W2);
   RRF_ALLOC(red, p->sz.red);
   RRF_ALLOC(rowj, p->sz.rowj);

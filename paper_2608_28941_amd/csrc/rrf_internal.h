@@ -106,6 +106,44 @@ hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s);
 struct PanelShape { int bp, rpt, G; int64_t rows_pad; };
 bool panel_shape(int64_t m, int b, int num_cus, int target_wgs, PanelShape* out);
 hipError_t launch_panel(const PanelArgs& a, const PanelShape& sh, hipStream_t s);
+// Panel by tall-skinny QR + Householder reconstruction (tsqr.hip).  Leaves
+// factor kTsqrLeafRpt * (256 / bp) rows each; tree nodes factor
+// kTsqrNodeRows stacked rows (kTsqrNodeRows / bp children).
+constexpr int kTsqrLeafRpt = 64;
+constexpr int kTsqrNodeRows = 256;
+constexpr int kTsqrMaxLev = 8;
+struct TsqrShape {
+  int bp, F, nlev;
+  int G[kTsqrMaxLev];          // nodes per level (G[0]: leaves)
+  int64_t scratch_elems;       // binary64 scratch the launch needs
+  int64_t rows_pad;            // rows of Y the leaves cover (V is written there)
+};
+struct TsqrLevelArgs {
+  const double* in; int64_t ldin; int64_t in_rows;  // rows >= in_rows read as 0
+  double* V; int64_t ldv;      // node V blocks (RW rows each)
+  double* M;                   // T V_top^T per node (BP x BP, column-major)
+  double* R; int64_t ldr;      // R of node w at rows [w BP, (w + 1) BP)
+  int b;
+};
+struct TsqrBackArgs {
+  const double* Vleaf; int64_t ldvl;
+  const double* Mleaf;
+  int nlev, F; int64_t rwi;
+  const double* Vlev[kTsqrMaxLev]; int64_t ldvlev[kTsqrMaxLev];
+  const double* Mlev[kTsqrMaxLev];
+  double* Q; int64_t ldq; int64_t m;
+};
+struct HrArgs {
+  double* Q; int64_t ldq; int64_t m; int b;   // explicit Q in, V out (in place)
+  double* Tm; int64_t ldt; double* tau;
+  double* Uinv;                                // BP x BP scratch
+};
+bool tsqr_shape(int64_t m, int b, TsqrShape* out);
+// Y (a.Y, read and overwritten: the leaves keep their reflectors there),
+// outputs a.V, a.Tm, a.tau as launch_panel; a.m, a.b.
+hipError_t launch_panel_tsqr(const PanelArgs& a, const TsqrShape& sh, double* scratch,
+                             hipStream_t s);
+
 // Look-ahead: the update (store, sample width qp) and the panel of the next
 // block in one launch; supported when bp == qp == the panel's padded width.
 bool update_panel_supported(int bp, int qp, const PanelShape& sh);

@@ -90,6 +90,14 @@ def test_scaled_workloads(name, m, n, b, tol):
     _check_against_live_oracle(w, W.build_matrix(w))
 
 
+@pytest.mark.parametrize("name,m,n,b,tol", [SCALED[0], SCALED[2], SCALED[3], SCALED[5]])
+def test_scaled_workloads_tsqr_panel(monkeypatch, name, m, n, b, tol):
+    # Same bar with the tall-skinny QR panel (chosen at plan creation).
+    monkeypatch.setenv("RRF_PANEL", "tsqr")
+    w = W.scaled(name, m, n, block_b=b, tol=tol)
+    _check_against_live_oracle(w, W.build_matrix(w))
+
+
 @pytest.mark.parametrize("name", W.GAP_INPUTS)
 def test_gap_inputs(name):
     w = W.WORKLOADS[name]

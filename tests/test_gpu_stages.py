@@ -2,7 +2,9 @@
 
 * sketch  -- bit-exact against oracle.normal_v1 (integer-decided bits and a
              fixed sequence of correctly rounded binary64 operations);
-* panel   -- V, tau, T against the oracle's geqr2 / larft on the same panel;
+* panel   -- V, tau, T against the oracle's geqr2 / larft on the same panel,
+             for both panel algorithms (column by column, and tall-skinny QR
+             with Householder reconstruction);
 * larfb   -- block reflector application against the oracle's reflector-by-
              reflector application (both directions).
 Tolerances for the floating-point stages are relative to the problem scale
@@ -41,10 +43,13 @@ PANEL_CASES = [(500, 16, 1), (64, 64, 2), (1000, 37, 3), (4096, 32, 4),
                (16384, 64, 5), (300, 5, 6), (131072, 32, 7)]
 
 
+@pytest.mark.parametrize("mode", ["grid", "tsqr"])
 @pytest.mark.parametrize("dtype", [np.float64, np.float32])
 @pytest.mark.parametrize("m,b,seed", PANEL_CASES)
-def test_panel_qr_matches_oracle(dtype, m, b, seed):
-    say(f"panel dtype={np.dtype(dtype).name} m={m} b={b}")
+def test_panel_qr_matches_oracle(monkeypatch, mode, dtype, m, b, seed):
+    # The panel algorithm is chosen when the plan is created.
+    monkeypatch.setenv("RRF_PANEL", mode)
+    say(f"panel mode={mode} dtype={np.dtype(dtype).name} m={m} b={b}")
     Y = W.random_graded(m, b, dtype, seed, decay=1e-2)
     V_o, tau_o = oracle.geqr2(Y.astype(np.float64))
     T_o = oracle.larft(V_o, tau_o)
