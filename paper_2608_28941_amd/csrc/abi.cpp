@@ -159,6 +159,27 @@ int upd_splits(int64_t mr, int64_t n, int num_cus) {
   return (int)std::max<int64_t>(s, 1);
 }
 
+// Column splits of the fused update + panel launch.  The panel holds G
+// workgroup slots for most of the launch, and the update's workgroups run in
+// rounds over the free slots; the split count that minimises rounds x
+// columns per split avoids a nearly empty last round (fewest splits on ties:
+// less partial-sample traffic).
+int upd_splits_fused(int64_t mr, int64_t n, int64_t free_slots) {
+  const int64_t row_wgs = std::max<int64_t>(ceil_div(mr, kUpdRows), 1);
+  const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(kMaxUpdSplits, n / 256));
+  const int64_t slots = std::max<int64_t>(free_slots, 1);
+  int best = 1;
+  double best_cost = 1e300;
+  for (int64_t sp = 1; sp <= smax; ++sp) {
+    const double cost = (double)ceil_div(row_wgs * sp, slots) / (double)sp;
+    if (cost < best_cost * (1.0 - 1e-9)) {
+      best_cost = cost;
+      best = (int)sp;
+    }
+  }
+  return best;
+}
+
 int red_splits(int64_t mr, int64_t n, int num_cus) {
   const int64_t col_wgs = ceil_div(n, kRedCols);
   int64_t s = ceil_div(4 * (int64_t)num_cus, std::max<int64_t>(col_wgs, 1));
@@ -466,13 +487,19 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     ua.W = (T*)p->W; ua.ldw = bp; ua.Om = Om; ua.ldo = kOmLd; ua.qp = q_s;
     ua.P = Yp; ua.ldp = ldb; ua.split_stride = ldb * 64; ua.s0 = bi;
     ua.normpart = p->normpart;
-    const int su0 = upd_splits(mp, n, p->num_cus);
+    const bool fused = panel_ready && update_panel_supported(bp, q_s, pan_shape);
+    int su0 = upd_splits(mp, n, p->num_cus);
+    if (fused) {
+      const int occ = update_panel_occupancy<T>(pan_shape);
+      if (occ > 0)
+        su0 = upd_splits_fused(mp, n, (int64_t)occ * p->num_cus - pan_shape.G);
+    }
     ua.cols_per_split = round_up(ceil_div(n, su0), kUpdChunk);
     const int su = (int)ceil_div(n, ua.cols_per_split);
     const double upd_flops = 2.0 * mp * n * bi + 2.0 * (mp - bi) * n * b_s;
     if (panel_ready) {
       pan.epoch_base = next_epoch(p);
-      if (update_panel_supported(bp, q_s, pan_shape)) {
+      if (fused) {
         RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops + pan_flops,
                    2.0 * e * mp * n + pan_bytes,
                    launch_update_panel<T>(ua, su, pan, pan_shape, s));

@@ -50,7 +50,44 @@ hipError_t up_rpt(const UpdateArgs<T>& ua, int nsplit, const PanelArgs& pa,
   return hipErrorNotSupported;
 }
 
+template <typename T, int BP, int RPT>
+int up_occ() {
+  static const int occ = [] {
+    int o = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &o, reinterpret_cast<const void*>(update_panel_kernel<T, BP, RPT>), 256, 0) != hipSuccess)
+      o = 0;
+    return o;
+  }();
+  return occ;
+}
+
+template <typename T, int BP>
+int up_occ_rpt(int rpt) {
+  switch (rpt) {
+    case 4: if constexpr ((kPanelThreads / BP) * 4 >= BP) return up_occ<T, BP, 4>(); break;
+    case 8: if constexpr ((kPanelThreads / BP) * 8 >= BP) return up_occ<T, BP, 8>(); break;
+    case 16: return up_occ<T, BP, 16>();
+    case 32: return up_occ<T, BP, 32>();
+    case 64: return up_occ<T, BP, 64>();
+  }
+  return 0;
+}
+
 }  // namespace
+
+template <typename T>
+int update_panel_occupancy(const PanelShape& sh) {
+  switch (sh.bp) {
+    case 16: return up_occ_rpt<T, 16>(sh.rpt);
+    case 32: return up_occ_rpt<T, 32>(sh.rpt);
+    case 64: return up_occ_rpt<T, 64>(sh.rpt);
+  }
+  return 0;
+}
+
+template int update_panel_occupancy<float>(const PanelShape&);
+template int update_panel_occupancy<double>(const PanelShape&);
 
 bool update_panel_supported(int bp, int qp, const PanelShape& sh) {
   return bp > 0 && bp == qp && bp == sh.bp;

@@ -95,19 +95,21 @@ __device__ __forceinline__ void panel_body(const PanelArgs& a, const int w) {
   constexpr int GR = kPanelThreads / BP;
   constexpr int RW = GR * RPT;
   static_assert(RW >= BP, "rows 0..b-1 must sit in workgroup 0");
-  __shared__ double xs[RW];
-  __shared__ double rowj_s[BP];
-  __shared__ double red_l[GR][BP];   // step partials of this workgroup
-  __shared__ double red_r[GR][BP];   // sums of the gathered partials
-  __shared__ double tot[BP], rj[BP];
-  __shared__ double Tl[BP][BP + 1];
-  __shared__ double Ej[BP];          // v_p^T v_j, p < j, of the last step
+  static_assert(64 % BP == 0, "a wavefront holds whole row groups");
+  __shared__ double xs[RW];           // column j below the diagonal, by row
+  __shared__ double red_l[2][GR][BP]; // step partials of this workgroup, by parity
+  __shared__ double red_r[GR][BP];    // sums of the gathered partials
+  __shared__ double rj[BP];           // row j of every column
+  __shared__ double Gm[BP][BP + 1];   // Gm[p][c] = v_p^T v_c, p < c (T workgroup)
   __shared__ double tau_s[BP];
 
   const int t = threadIdx.x;
   const int k = t % BP, g = t / BP;
   const int64_t base = (int64_t)w * RW;
   const int b = a.b;
+  // The last workgroup collects V^T V and builds T at the end; workgroup 0
+  // (which publishes row j every step) has no extra work.
+  const bool tw = (w == a.G - 1);
 
   // The gathered panel has G * RW rows and BP columns, zero outside (m, b),
   // so the RPT loads are unconditional and all in flight together.
@@ -117,26 +119,31 @@ __device__ __forceinline__ void panel_body(const PanelArgs& a, const int w) {
 #pragma unroll
     for (int q = 0; q < RPT; ++q) col[q] = Yk[GR * q];
   }
+  if (tw) {
+    for (int idx = t; idx < BP * (BP + 1); idx += kPanelThreads) (&Gm[0][0])[idx] = 0.0;
+    if (t < BP) tau_s[t] = 0.0;
+  }
 
-  // Column jj of T (workgroup 0) from Ej and tau_s: the forward columnwise
-  // recursion T[:jj, jj] = -tau_jj T[:jj, :jj] (V^T v_jj).
-  auto t_column = [&](int jj) {
-    if (t < jj) {
-      double acc = 0.0;
-      for (int p = t; p < jj; ++p) acc += Tl[t][p] * Ej[p];
-      Tl[t][jj] = -tau_s[jj] * acc;
-    } else if (t == jj) {
-      Tl[jj][jj] = tau_s[jj];
-    }
-  };
-
+  constexpr int QJ = (BP + GR - 1) / GR;   // registers that can hold rows < BP
   for (int j = 0; j < b; ++j) {
     const int par = j & 1;
-    // 1. Broadcast column j with its rows <= j zeroed: then every dot below
+    const unsigned epoch = a.epoch_base + (unsigned)j + 1u;
+    // 1. Row j of every column (final after step j - 1) sits in workgroup 0,
+    //    row group j % GR, register j / GR: publish it at once.
+    if (w == 0 && g == j % GR) {
+      const int qj = j / GR;
+      double v = 0.0;
+#pragma unroll
+      for (int q = 0; q < QJ; ++q) v = (q == qj) ? col[q] : v;
+      put_tagged(&a.rowj[(par * BP + k) * 2], v, epoch);
+    }
+    // 2. Broadcast column j with its rows <= j zeroed (then every dot below
     //    is over rows > j and the rank-1 update leaves rows <= j untouched,
-    //    with no per-row conditions.  Row j of every column sits in
-    //    workgroup 0 (row group j % GR, register j / GR).
-    constexpr int QJ = (BP + GR - 1) / GR;   // registers that can hold rows < BP
+    //    with no per-row conditions).  Each row group lies inside one
+    //    wavefront, whose lane k == j writes the group's rows and whose
+    //    lanes read them: LDS operations of a wavefront complete in order,
+    //    so no workgroup barrier is needed, and the next step's write comes
+    //    after this step's last read in the same order.
     if (k == j) {
       if (w == 0) {
 #pragma unroll
@@ -147,49 +154,38 @@ __device__ __forceinline__ void panel_body(const PanelArgs& a, const int w) {
         for (int q = 0; q < RPT; ++q) xs[g + GR * q] = col[q];
       }
     }
-    if (w == 0 && g == j % GR) {
-      const int qj = j / GR;
-      double v = 0.0;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    // 3. Partial dot of this thread's column with x (rows > j).
+    {
+      double d0 = 0.0, d1 = 0.0;
 #pragma unroll
-      for (int q = 0; q < QJ; ++q) v = (q == qj) ? col[q] : v;
-      rowj_s[k] = v;
+      for (int q = 0; q < RPT; q += 2) {
+        d0 += col[q] * xs[g + GR * q];
+        if (q + 1 < RPT) d1 += col[q + 1] * xs[g + GR * (q + 1)];
+      }
+      red_l[par][g][k] = d0 + d1;
     }
     __syncthreads();
-    // 2. Partial dot of this thread's column with x (rows > j).
-    double d = 0.0;
-#pragma unroll
-    for (int q = 0; q < RPT; ++q) d += col[q] * xs[g + GR * q];
-    red_l[g][k] = d;
-    __syncthreads();
-    // 3. Workgroup partial to global memory as epoch-tagged words.  While
-    //    the other workgroups catch up, workgroup 0 finishes the previous
-    //    column of T.
-    const unsigned epoch = a.epoch_base + (unsigned)j + 1u;
+    // 4. Workgroup partial to global memory as epoch-tagged words.
     if (t < BP) {
       double s = 0.0;
-      for (int gg = 0; gg < GR; ++gg) s += red_l[gg][t];
+#pragma unroll
+      for (int gg = 0; gg < GR; ++gg) s += red_l[par][gg][t];
       put_tagged(&a.red[(((int64_t)par * a.G + w) * BP + t) * 2], s, epoch);
-      if (w == 0) put_tagged(&a.rowj[(par * BP + t) * 2], rowj_s[t], epoch);
     }
-    if (w == 0 && j > 0) t_column(j - 1);
-    // 4. Every workgroup sums all partials in the same fixed order, polling
-    //    each batch until it is complete; row j is read the same way.
+    // 5. Every workgroup sums all partials in the same fixed order, polling
+    //    each batch until it is complete; threads t < BP read row j in the
+    //    first batch.
     {
       const int kk = t % BP, sub = t / BP;
       const u64* rp = a.red + ((int64_t)par * a.G * BP + kk) * 2;
+      const u64* rq = &a.rowj[(par * BP + kk) * 2];
       unsigned spins = 0;
-      if (t < BP) {
-        const u64* q = &a.rowj[(par * BP + t) * 2];
-        u64 hi = get_word(q), lo = get_word(q + 1);
-        while (!(tagged(hi, epoch) && tagged(lo, epoch)) && keep_waiting(&spins, a.st)) {
-          hi = get_word(q);
-          lo = get_word(q + 1);
-        }
-        rj[t] = untag(hi, lo);
-      }
       double s = 0.0;
       for (int w0 = sub; w0 < a.G; w0 += 16 * GR) {
-        u64 hi[16], lo[16];
+        const bool row = (w0 == 0);   // only sub == 0 starts at 0
+        u64 hi[16], lo[16], rh = 0, rl = 0;
         bool ok;
         do {
 #pragma unroll
@@ -199,7 +195,11 @@ __device__ __forceinline__ void panel_body(const PanelArgs& a, const int w) {
             hi[u] = get_word(q);
             lo[u] = get_word(q + 1);
           }
-          ok = true;
+          if (row) {
+            rh = get_word(rq);
+            rl = get_word(rq + 1);
+          }
+          ok = !row || (tagged(rh, epoch) && tagged(rl, epoch));
 #pragma unroll
           for (int u = 0; u < 16; ++u)
             ok = ok && tagged(hi[u], epoch) && tagged(lo[u], epoch);
@@ -207,47 +207,46 @@ __device__ __forceinline__ void panel_body(const PanelArgs& a, const int w) {
 #pragma unroll
         for (int u = 0; u < 16; ++u)
           if (w0 + u * GR < a.G) s += untag(hi[u], lo[u]);
+        if (row) rj[kk] = untag(rh, rl);
       }
-      // red_r, not red_l: threads of other wavefronts may still be
-      // reading red_l in step 3.
       red_r[sub][kk] = s;
     }
     __syncthreads();
-    if (t < BP) {
-      double s = 0.0;
-      for (int gg = 0; gg < GR; ++gg) s += red_r[gg][t];
-      tot[t] = s;
+    // 6. Totals and dlarfg scalars (identical in every thread of every
+    //    workgroup: the same sums in the same order).
+    double tk = 0.0, tj = 0.0;
+#pragma unroll
+    for (int gg = 0; gg < GR; ++gg) {
+      tk += red_r[gg][k];
+      tj += red_r[gg][j];
     }
-    __syncthreads();
-    // 5. dlarfg scalars (identical in every workgroup).
-    const double alpha = rj[j];
-    const double xi2 = tot[j];
+    const double alpha = rj[j], rk = rj[k];
     double tau_j = 0.0, scale = 0.0;
-    if (xi2 != 0.0) {
-      const double nrm = sqrt(alpha * alpha + xi2);
+    if (tj != 0.0) {
+      const double nrm = sqrt(alpha * alpha + tj);
       const double beta = (alpha >= 0.0) ? -nrm : nrm;
       tau_j = (beta - alpha) / beta;
       scale = 1.0 / (alpha - beta);
     }
-    // 6. v_j = x * scale below the diagonal (rows <= j of column j are never
+    // 7. v_j = x * scale below the diagonal (rows <= j of column j are never
     //    read again); trailing columns y_k -= tau_j (v_j^T y_k) v_j with
-    //    v_j^T y_k = y_k[j] + scale * dot_k (xs is zero on rows <= j).
+    //    v_j^T y_k = y_k[j] + scale * dot_k (xs is zero on rows <= j; row j
+    //    of y_k, an entry of R, is not needed again).
+    const double wk = rk + scale * tk;
     if (k == j) {
 #pragma unroll
       for (int q = 0; q < RPT; ++q) col[q] = col[q] * scale;
     } else if (k > j && k < b) {
-      const double fs = tau_j * (rj[k] + scale * tot[k]) * scale;
+      const double fs = tau_j * wk * scale;
 #pragma unroll
       for (int q = 0; q < RPT; ++q) col[q] = col[q] - fs * xs[g + GR * q];
     }
-    // 7. Save v_p^T v_j = V[j, p] + scale * dot_p (p < j) for T (workgroup 0).
-    if (w == 0) {
-      if (t < j) Ej[t] = rj[t] + scale * tot[t];
-      else if (t == j) tau_s[j] = tau_j;
+    // 8. v_p^T v_j = V[j, p] + scale * dot_p (p < j), for T.
+    if (tw && g == 0) {
+      if (k < j) Gm[k][j] = wk;
+      else if (k == j) tau_s[j] = tau_j;
     }
-    __syncthreads();
   }
-  if (w == 0 && b > 0) t_column(b - 1);
   __syncthreads();
 
   // Outputs: V with explicit unit diagonal and zeros above / beyond b.
@@ -260,12 +259,29 @@ __device__ __forceinline__ void panel_body(const PanelArgs& a, const int w) {
       a.V[r + k * a.ldv] = v;
     }
   }
-  if (w == 0) {
-    for (int idx = t; idx < BP * BP; idx += kPanelThreads) {
-      const int i = idx % BP, jj = idx / BP;
-      a.Tm[i + (int64_t)jj * a.ldt] = (jj < b && i <= jj) ? Tl[i][jj] : 0.0;
+  // T (Eq. (4)) from V^T V and tau: with U = striu(V^T V), T is the inverse
+  // of diag(1/tau) + U, i.e. T[c][c] = tau_c and, for i < c,
+  // T[i][c] = -tau_i sum_{i < p <= c} U[i][p] T[p][c] (written with tau as
+  // a factor, so tau_i = 0 gives a zero row: H_i = I).  Thread c solves
+  // column c by back substitution in registers.  U is zero outside the
+  // written entries, and T[p][c] = 0 for p > c, so the full sums are exact.
+  if (tw && t < BP) {
+    const int c = t;
+    double tc[BP];
+#pragma unroll
+    for (int i = BP - 1; i >= 0; --i) {
+      double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+      for (int p = i + 1; p < BP; p += 2) {
+        s0 += Gm[i][p] * tc[p];
+        if (p + 1 < BP) s1 += Gm[i][p + 1] * tc[p + 1];
+      }
+      const double ti = tau_s[i];
+      tc[i] = (c < b && i < c) ? -ti * (s0 + s1) : ((c < b && i == c) ? ti : 0.0);
     }
-    if (t < b) a.tau[t] = Tl[t][t];
+#pragma unroll
+    for (int i = 0; i < BP; ++i) a.Tm[i + (int64_t)c * a.ldt] = tc[i];
+    if (c < b) a.tau[c] = tau_s[c];
   }
 }
 

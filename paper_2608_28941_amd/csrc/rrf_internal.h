@@ -151,6 +151,9 @@ template <typename T>
 hipError_t launch_update_panel(const UpdateArgs<T>& ua, int nsplit,
                                const PanelArgs& pa, const PanelShape& sh,
                                hipStream_t s);
+// Workgroups of that launch resident per compute unit (0 if unknown).
+template <typename T>
+int update_panel_occupancy(const PanelShape& sh);
 // Ysum[r + k * ldy] = sum_s P_s[r + k * ldp] for r < m, k < b; 0 elsewhere
 // for r < rows_pad, k < bp (binary64).
 template <typename T>
