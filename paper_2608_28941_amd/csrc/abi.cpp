@@ -36,16 +36,18 @@ constexpr int kMaxRedSplits = 32;
 constexpr int kOmLd = 64;         // Omega stored [c][q] with row length 64
 constexpr int kPanelGrid = 0;      // column-by-column panel, one grid reduction per column
 constexpr int kPanelTsqr = 1;      // tall-skinny QR + Householder reconstruction
+constexpr int kPanelGram = 2;      // column recurrence from the Gram matrix, one exchange per sweep
+constexpr int kPanelAuto = 3;      // kPanelGram for blocks of <= 32 columns, else kPanelGrid
 constexpr int kTLd = 64;          // T stored like geqrt's T: 64 rows
 
 struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
-      rowj, st, trace, Zpart2, W2, tsqr;
+      rowj, st, trace, Zpart2, W2, tsqr, gx;
   size_t total() const {
     return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
-           normpart + red + rowj + st + trace + Zpart2 + W2 + tsqr;
+           normpart + red + rowj + st + trace + Zpart2 + W2 + tsqr + gx;
   }
 };
 
@@ -75,6 +77,7 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   // Panel partials: two epoch-tagged 64-bit words per value.
   z.red = (size_t)2 * kMaxPanelWGs * 64 * 2 * 8;
   z.rowj = (size_t)2 * 64 * 2 * 8;
+  z.gx = (size_t)(kGramPartWords + kGramSumWords) * 8;
   z.st = sizeof(DevState);
   z.trace = (size_t)2 * std::max<int64_t>(z.kcap, 1) * 8;
   // Look-ahead: Q_i^T applied to the m x b sample (64 columns at most).
@@ -105,10 +108,10 @@ struct rrf_plan {
   void *Bws, *Ypart, *Om, *Zpart, *W, *Q, *Q64;
   double *Zpart2, *W2;       // scratch of the look-ahead's small reflector application
   double* tsqr;              // scratch of the tall-skinny QR panel
-  int panel_mode;            // kPanelGrid or kPanelTsqr
+  int panel_mode;            // kPanelGrid, kPanelTsqr, kPanelGram or kPanelAuto
   double *V, *Tm, *tau, *Ysum;
   double *normpart, *trace_trail_d, *trace_sub_d;
-  unsigned long long *red, *rowj;
+  unsigned long long *red, *rowj, *gx;
   DevState* st;
   DevState* st_host;
   int stop_mode, timing, panel_target;
@@ -253,11 +256,29 @@ hipError_t read_state(rrf_plan* p) {
 
 // Panel QR of the gathered panel pa.Y (m x b) into pa.V, pa.Tm, pa.tau with
 // the plan's panel algorithm (pa.Y is overwritten by the tall-skinny QR).
+// The panel algorithm for a block of b columns.  Narrow panels take the Gram
+// form (its column steps are cheap at 32 columns and it exchanges once per
+// sweep); 64-column panels take the column-by-column grid, which the
+// look-ahead hides inside the update.
+int panel_alg(const rrf_plan* p, int64_t b) {
+  if (p->panel_mode != kPanelAuto) return p->panel_mode;
+  return pad16(b) <= 32 ? kPanelGram : kPanelGrid;
+}
 bool panel_fits(rrf_plan* p, int64_t m, int b, PanelShape* sh) {
+  if (panel_alg(p, b) == kPanelGram) return gram_panel_shape(m, b, p->num_cus, sh);
   return panel_shape(m, b, p->num_cus, p->panel_target, sh);
 }
 hipError_t run_panel(rrf_plan* p, PanelArgs& pa, const PanelShape& sh, hipStream_t s) {
-  if (p->panel_mode == kPanelTsqr) {
+  const int alg = panel_alg(p, pa.b);
+  if (alg == kPanelGram) {
+    GramPanelArgs ga{};
+    ga.p = pa;
+    ga.p.epoch_base = next_epoch(p);
+    ga.part = p->gx;
+    ga.sums = p->gx + kGramPartWords;
+    return launch_panel_gram(ga, sh, s);
+  }
+  if (alg == kPanelTsqr) {
     TsqrShape ts;
     if (!tsqr_shape(pa.m, pa.b, &ts)) return hipErrorInvalidValue;
     return launch_panel_tsqr(pa, ts, p->tsqr, s);
@@ -365,7 +386,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   // workgroups of the update's own launch while the rest update B.
   // It pays when the panel grid is small: a panel of more than a quarter of
   // the compute units takes too many slots from the update it runs beside.
-  bool la = p->lookahead != 0 && p->panel_mode == kPanelGrid && kcap > b;
+  bool la = p->lookahead != 0 && panel_alg(p, b) == kPanelGrid && kcap > b;
   if (la) {
     PanelShape sh1;
     la = panel_shape(m - b, (int)std::min(b, kcap - b), p->num_cus, p->panel_target, &sh1) &&
@@ -385,7 +406,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       panel_ready = false;
     } else {
       PanelShape sh;
-      if (!panel_shape(mp, (int)bi, p->num_cus, p->panel_target, &sh)) return RRF_ERR_SHAPE;
+      if (!panel_fits(p, mp, (int)bi, &sh)) return RRF_ERR_SHAPE;
       RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mp * bi * ysplits + 8.0 * mp * bi,
                  launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
                                         (int)bi, bp, sh.rows_pad, p->Ysum,
@@ -593,7 +614,7 @@ rrf_status panel_stage(rrf_plan* p, const T* Y, int64_t m, int64_t b,
                        int64_t ldy, T* Vout, int64_t ldv, T* Tout, int64_t ldt,
                        T* tauout) {
   PanelShape sh;
-  if (!panel_shape(m, (int)b, p->num_cus, p->panel_target, &sh)) return RRF_ERR_SHAPE;
+  if (!panel_fits(p, m, (int)b, &sh)) return RRF_ERR_SHAPE;
   hipStream_t s = p->stream;
   hipError_t e0 = launch_gather_panel<T>(Y, ldy, 0, 1, m, (int)b, sh.bp,
                                          sh.rows_pad, p->Ysum, p->sz.ldysum, s);
@@ -688,12 +709,17 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   // overlap); the default factors the next panel during the update.
   p->lookahead = 1;
   if (const char* la = std::getenv("RRF_LOOKAHEAD")) p->lookahead = std::atoi(la) != 0;
-  // RRF_PANEL=tsqr selects the tall-skinny QR panel with Householder
-  // reconstruction; the default is the column-by-column panel (one grid-wide
-  // reduction per column), the only one the look-ahead overlaps.
-  p->panel_mode = kPanelGrid;
-  if (const char* pm = std::getenv("RRF_PANEL"))
+  // RRF_PANEL selects the panel algorithm: "grid" (column by column, one
+  // grid-wide reduction per column; the only one the look-ahead overlaps),
+  // "gram" (the same reflectors from the Gram matrix, one grid exchange per
+  // sweep of columns), "tsqr" (tall-skinny QR with Householder
+  // reconstruction); the default picks gram or grid by the block width.
+  p->panel_mode = kPanelAuto;
+  if (const char* pm = std::getenv("RRF_PANEL")) {
     if (std::strcmp(pm, "tsqr") == 0) p->panel_mode = kPanelTsqr;
+    else if (std::strcmp(pm, "gram") == 0) p->panel_mode = kPanelGram;
+    else if (std::strcmp(pm, "grid") == 0) p->panel_mode = kPanelGrid;
+  }
   if (hipGetDevice(&p->device) != hipSuccess ||
       hipDeviceGetAttribute(&p->num_cus, hipDeviceAttributeMultiprocessorCount,
                             p->device) != hipSuccess) {
@@ -702,8 +728,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   }
   // The first panel has m_max rows; it must fit the register-resident panel.
   PanelShape sh;
-  if (!panel_shape(std::max(m_max, block_b_max), (int)block_b_max, p->num_cus,
-                   p->panel_target, &sh)) {
+  if (!panel_fits(p, std::max(m_max, block_b_max), (int)block_b_max, &sh)) {
     free_plan(p);
     return RRF_ERR_SHAPE;
   }
@@ -735,6 +760,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   RRF_ALLOC(W2, p->sz.W2);
   RRF_ALLOC(red, p->sz.red);
   RRF_ALLOC(rowj, p->sz.rowj);
+  RRF_ALLOC(gx, p->sz.gx);
   RRF_ALLOC(st, p->sz.st);
   RRF_ALLOC(trace_trail_d, p->sz.trace / 2);
   RRF_ALLOC(trace_sub_d, p->sz.trace / 2);
@@ -747,6 +773,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   }
   if (e == hipSuccess) e = hipMemsetAsync(p->red, 0, p->sz.red, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->rowj, 0, p->sz.rowj, p->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(p->gx, 0, p->sz.gx, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->st, 0, p->sz.st, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->Om, 0, p->sz.Om, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->V, 0, p->sz.V, p->stream);

@@ -144,6 +144,22 @@ bool tsqr_shape(int64_t m, int b, TsqrShape* out);
 hipError_t launch_panel_tsqr(const PanelArgs& a, const TsqrShape& sh, double* scratch,
                              hipStream_t s);
 
+// Panel from the Gram matrix (one grid exchange per sweep of columns); the
+// scratch holds 2 x G x NS tagged partial sums (part) and 2 x (NS + bp^2)
+// tagged sums (sums), NS = 256 x the upper-triangle 16 x 16 tiles of a
+// bp x bp matrix (2560 for bp = 64), zeroed once.
+constexpr int kMaxGramWGs = 256;
+constexpr int64_t kGramSlots = 10 * 256;
+constexpr int64_t kGramPartWords = 2LL * kMaxGramWGs * kGramSlots * 2;
+constexpr int64_t kGramSumWords = 2LL * (kGramSlots + 64 * 64) * 2;
+struct GramPanelArgs {
+  PanelArgs p;                 // Y, ldy, m, b, V, Tm, tau, st, G, epoch_base
+  unsigned long long* part;
+  unsigned long long* sums;
+};
+bool gram_panel_shape(int64_t m, int b, int num_cus, PanelShape* out);
+hipError_t launch_panel_gram(const GramPanelArgs& a, const PanelShape& sh, hipStream_t s);
+
 // Look-ahead: the update (store, sample width qp) and the panel of the next
 // block in one launch; supported when bp == qp == the panel's padded width.
 bool update_panel_supported(int bp, int qp, const PanelShape& sh);

@@ -98,6 +98,21 @@ def test_scaled_workloads_tsqr_panel(monkeypatch, name, m, n, b, tol):
     _check_against_live_oracle(w, W.build_matrix(w))
 
 
+@pytest.mark.parametrize("name,m,n,b,tol", SCALED)
+def test_scaled_workloads_gram_panel(monkeypatch, name, m, n, b, tol):
+    # Same bar with the Gram-matrix panel (chosen at plan creation).
+    monkeypatch.setenv("RRF_PANEL", "gram")
+    w = W.scaled(name, m, n, block_b=b, tol=tol)
+    _check_against_live_oracle(w, W.build_matrix(w))
+
+
+@pytest.mark.parametrize("name", W.GAP_INPUTS)
+def test_gap_inputs_gram_panel(monkeypatch, name):
+    monkeypatch.setenv("RRF_PANEL", "gram")
+    w = W.WORKLOADS[name]
+    _check_against_live_oracle(w, W.build_matrix(w), gap=True)
+
+
 @pytest.mark.parametrize("name", W.GAP_INPUTS)
 def test_gap_inputs(name):
     w = W.WORKLOADS[name]

@@ -3,8 +3,9 @@
 * sketch  -- bit-exact against oracle.normal_v1 (integer-decided bits and a
              fixed sequence of correctly rounded binary64 operations);
 * panel   -- V, tau, T against the oracle's geqr2 / larft on the same panel,
-             for both panel algorithms (column by column, and tall-skinny QR
-             with Householder reconstruction);
+             for the three panel algorithms (column by column, from the
+             Gram matrix with one exchange per sweep, and tall-skinny QR with
+             Householder reconstruction);
 * larfb   -- block reflector application against the oracle's reflector-by-
              reflector application (both directions).
 Tolerances for the floating-point stages are relative to the problem scale
@@ -43,7 +44,7 @@ PANEL_CASES = [(500, 16, 1), (64, 64, 2), (1000, 37, 3), (4096, 32, 4),
                (16384, 64, 5), (300, 5, 6), (131072, 32, 7)]
 
 
-@pytest.mark.parametrize("mode", ["grid", "tsqr"])
+@pytest.mark.parametrize("mode", ["grid", "gram", "tsqr"])
 @pytest.mark.parametrize("dtype", [np.float64, np.float32])
 @pytest.mark.parametrize("m,b,seed", PANEL_CASES)
 def test_panel_qr_matches_oracle(monkeypatch, mode, dtype, m, b, seed):
