@@ -68,6 +68,50 @@ def test_panel_qr_matches_oracle(monkeypatch, mode, dtype, m, b, seed):
     assert np.all(np.triu(V, 1) == 0) and np.all(np.diag(V) == 1)
 
 
+def _rank_deficient(m, b, r, seed):
+    g = np.random.default_rng(seed)
+    return np.asfortranarray(g.standard_normal((m, r)) @ g.standard_normal((r, b)))
+
+
+@pytest.mark.parametrize("mode", ["grid", "gram", "tsqr"])
+@pytest.mark.parametrize("case", ["graded1e-8", "graded1e-13", "rank12of32", "zero_cols"])
+def test_panel_qr_hard_panels(monkeypatch, mode, case):
+    """Ill-conditioned and rank-deficient panels: whatever route computes
+    the inner products (the Gram route downdates norms and must re-form F
+    when they cancel), the reflectors stay orthogonal and Q^T Y is upper
+    triangular to binary64 roundoff.  Q = I - V T V^T is orthogonal iff
+    M = T^T (V^T V) T - T - T^T vanishes (Q^T Q - I = V M V^T)."""
+    monkeypatch.setenv("RRF_PANEL", mode)
+    if case == "graded1e-8":
+        Y = W.random_graded(4096, 64, np.float64, 11, decay=1e-8)
+    elif case == "graded1e-13":
+        Y = W.random_graded(16384, 32, np.float64, 12, decay=1e-13)
+    elif case == "rank12of32":
+        Y = _rank_deficient(2000, 32, 12, 13)
+    else:
+        Y = W.random_graded(3000, 48, np.float64, 14, decay=1e-3)
+        Y[:, [5, 17, 40]] = 0.0
+    m, b = Y.shape
+    say(f"hard panel mode={mode} case={case} m={m} b={b}")
+    with rrf.Plan(torch.float64, m, b, b) as p:
+        V, T, tau = p.panel_qr(to_dev(Y))
+        V, T, tau = to_host(V), to_host(T), to_host(tau)
+    assert np.all(np.isfinite(V)) and np.all(np.isfinite(T))
+    assert np.all(np.triu(V, 1) == 0) and np.all(np.diag(V) == 1)
+    G = V.T @ V
+    M = T.T @ G @ T - T - T.T
+    assert np.linalg.norm(M) * np.linalg.norm(V, 2) ** 2 < 1e-12
+    R = Y - V @ (T.T @ (V.T @ Y))           # Q^T Y
+    ny = np.linalg.norm(Y)
+    assert np.linalg.norm(R[b:, :]) <= 1e-13 * ny
+    assert np.linalg.norm(np.tril(R[:b, :], -1)) <= 1e-13 * ny
+    if case == "zero_cols":
+        # A zero column below the diagonal gives tau = 0 only if nothing
+        # remains of it after the previous reflectors; the property checks
+        # above are what must hold.
+        assert np.all(tau >= 0) and np.all(tau <= 2)
+
+
 @pytest.mark.parametrize("dtype", [np.float64, np.float32])
 @pytest.mark.parametrize("trans", [True, False])
 @pytest.mark.parametrize("m,n,b,seed", [(200, 100, 16, 1), (777, 333, 45, 2),
