@@ -66,36 +66,39 @@ struct GramGeom {
   }
 };
 
-template <int BP, int RPT>
+template <int BP, int RPT, int NT>
 struct GramLds {
-  static constexpr int GR = kPanelThreads / BP;
+  static constexpr int GR = NT / BP;
   double S[BP][BP + 2];         // staged rows for the Gram sums
   double top[BP][BP + 2];       // rows 0..b-1 of X; above the diagonal of finished
                                 // rows p: v_p^T v_c (c > p), for T
   double xs[GR][RPT + 2];       // column j at each row group's rows
   double ujv[2][BP];            // column j of F, by step parity
-  double scal[2][4];            // recompute flag, tau, scale of the step, by parity
+  double fdiag[2];              // F[j+1][j+1] before step j, by parity
   double cw[BP], zv[BP], xt[BP], nu[BP], tau[BP];
   double colscale[BP];          // 1 / (alpha - beta) of finished columns, else 1
-  double red2[kPanelThreads];
+  double red2[NT];
 };
 
-template <int BP, int RPT>
-__global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs ga) {
+template <int BP, int RPT, int NT>
+__global__ __launch_bounds__(NT) void panel_gram_kernel(GramPanelArgs ga) {
   typedef GramGeom<BP> Geo;
-  constexpr int GR = kPanelThreads / BP;
+  constexpr int GR = NT / BP;
   constexpr int RW = GR * RPT;
   constexpr int QC = BP / GR;        // register slots per staged chunk of BP rows
-  constexpr int BS = BP / 16;        // F / top block per thread: BS x BS
+  constexpr int BC = BP / 16;        // F block per thread: BR rows x BC columns,
+  constexpr int BR = BP * BP / NT / BC;   // 16 blocks across, NT / 16 down
   constexpr int QJ = (BP + GR - 1) / GR;
-  constexpr int NTW = (Geo::NTL + 3) / 4;   // Gram tiles per wavefront
+  constexpr int NW = NT / 64;        // wavefronts
+  constexpr int NTW = (Geo::NTL + NW - 1) / NW;   // Gram tiles per wavefront
   static_assert(RPT % QC == 0 && RW >= BP, "panel shape");
-  __shared__ GramLds<BP, RPT> L;
+  static_assert(BR >= 1 && BR * BC * NT == BP * BP, "F blocks");
+  __shared__ GramLds<BP, RPT, NT> L;
 
   const PanelArgs& a = ga.p;
   const int t = threadIdx.x;
   const int k = t % BP, g = t / BP;           // register layout (column k, row group g)
-  const int bi = t / 16, bj = t % 16;         // F / top block (rows BS bi.., cols BS bj..)
+  const int bi = t / 16, bj = t % 16;         // F / top block (rows BR bi.., cols BC bj..)
   const int wv = t / 64, l16 = (t % 64) / 16, m16 = t % 16;   // MFMA lane roles
   const int w = (int)blockIdx.x;
   const int64_t base = (int64_t)w * RW;
@@ -108,11 +111,11 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
     for (int q = 0; q < RPT; ++q) col[q] = Yk[GR * q];
   }
   if (t < BP) L.colscale[t] = 1.0;
-  double Fr[BS][BS];
+  double Fr[BR][BC];
   int tti[NTW], ttj[NTW];
 #pragma unroll
   for (int x = 0; x < NTW; ++x) {
-    int r = wv + 4 * x;
+    int r = wv + NW * x;
     tti[x] = -1;
     ttj[x] = -1;
     for (int i = 0; i < Geo::N16; ++i) {
@@ -188,8 +191,8 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
       const int se = (NS + G - 1) / G;
       const int e0 = w * se;
       const int ne = max(0, min(NS, e0 + se) - e0);
-      const int nsub = max(1, min(16, kPanelThreads / max(ne, 1)));
-      const int per = kPanelThreads / nsub;
+      const int nsub = max(1, min(16, NT / max(ne, 1)));
+      const int per = NT / nsub;
       for (int p0 = 0; p0 < ne; p0 += per) {
         const int el = p0 + t % per, sub = t / per;
         double s = 0.0;
@@ -229,33 +232,33 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
     // Phase 3: every thread reads the sums of its F entries (and, the first
     // time, its entries of the top block).
     {
-      constexpr int NQ = BS * BS;
+      constexpr int NQ = BR * BC;
       unsigned spins = 0;
       auto fetch = [&](const bool topblk) __attribute__((always_inline)) {
         u64 hi[NQ], lo[NQ];
         bool ok;
         do {
 #pragma unroll
-          for (int i = 0; i < BS; ++i)
+          for (int i = 0; i < BR; ++i)
 #pragma unroll
-            for (int jj = 0; jj < BS; ++jj) {
-              const int r = BS * bi + i, c = BS * bj + jj;
+            for (int jj = 0; jj < BC; ++jj) {
+              const int r = BR * bi + i, c = BC * bj + jj;
               const int idx = (topblk && r < b) ? Geo::NSLOT + r * BP + c : Geo::slot(r, c);
               const u64* q = ga.sums + ((int64_t)par * Geo::NEX + idx) * 2;
-              hi[i * BS + jj] = get_word(q);
-              lo[i * BS + jj] = get_word(q + 1);
+              hi[i * BC + jj] = get_word(q);
+              lo[i * BC + jj] = get_word(q + 1);
             }
           ok = true;
 #pragma unroll
           for (int i = 0; i < NQ; ++i) ok = ok && tagged(hi[i], epoch) && tagged(lo[i], epoch);
         } while (!ok && keep_waiting(&spins, a.st));
 #pragma unroll
-        for (int i = 0; i < BS; ++i)
+        for (int i = 0; i < BR; ++i)
 #pragma unroll
-          for (int jj = 0; jj < BS; ++jj) {
-            const double v = untag(hi[i * BS + jj], lo[i * BS + jj]);
+          for (int jj = 0; jj < BC; ++jj) {
+            const double v = untag(hi[i * BC + jj], lo[i * BC + jj]);
             if (!topblk) Fr[i][jj] = v;
-            else L.top[BS * bi + i][BS * bj + jj] = (BS * bi + i < b) ? v : 0.0;
+            else L.top[BR * bi + i][BC * bj + jj] = (BR * bi + i < b) ? v : 0.0;
           }
       };
       fetch(false);
@@ -264,52 +267,60 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
   };
 
   // Exports for step jn (parity pn) by the owners of the entries: column jn
-  // of F and of the top block, top rows jn and jn + 1, and (owner of
-  // (jn, jn)) the step's dlarfg scalars and the recompute decision.
-  auto export_step = [&](const int jn, const int pn, const bool fresh) __attribute__((always_inline)) {
-    const int jb = jn / BS, jo = jn % BS;
-    // jo is the same in every thread: the branches below are uniform, and
-    // every register index is a constant (no dynamically indexed array).
+  // of F, and F[jn+1][jn+1] (the next pivot's norm before step jn).
+  auto export_step = [&](const int jn, const int pn) __attribute__((always_inline)) {
+    const int jb = jn / BC, jo = jn % BC;
+    const int j1r = (jn + 1) / BR, j1i = (jn + 1) % BR;
+    const int j1c = (jn + 1) / BC, j1o = (jn + 1) % BC;
+    // jo, j1i, j1o are the same in every thread: the branches below are
+    // uniform, and every register index is a constant (no dynamically
+    // indexed array).
     if (bj == jb) {
 #pragma unroll
-      for (int jj = 0; jj < BS; ++jj)
+      for (int jj = 0; jj < BC; ++jj)
         if (jj == jo)
 #pragma unroll
-          for (int i = 0; i < BS; ++i) L.ujv[pn][BS * bi + i] = Fr[i][jj];
-      if (bi == jb) {
-        double xn2 = 0.0;
+          for (int i = 0; i < BR; ++i) L.ujv[pn][BR * bi + i] = Fr[i][jj];
+    }
+    if (bi == j1r && bj == j1c) {
 #pragma unroll
-        for (int d = 0; d < BS; ++d)
-          if (d == jo) xn2 = Fr[d][d];
-        const double alpha = L.top[jn][jn];
-        const double nuj = L.nu[jn];
-        double flag = 0.0, tau_j = 0.0, scale = 0.0;
-        if (!fresh && nuj > 0.0 && !(xn2 >= kGramTheta * nuj)) {
-          flag = 1.0;
-        } else if (xn2 > 0.0) {
-          const double nrm = sqrt(alpha * alpha + xn2);
-          const double beta = (alpha >= 0.0) ? -nrm : nrm;
-          tau_j = (beta - alpha) / beta;
-          scale = 1.0 / (alpha - beta);
-        }
-        L.scal[pn][0] = flag;
-        L.scal[pn][1] = tau_j;
-        L.scal[pn][2] = scale;
-      }
+      for (int i = 0; i < BR; ++i)
+#pragma unroll
+        for (int jj = 0; jj < BC; ++jj)
+          if (i == j1i && jj == j1o) L.fdiag[pn] = Fr[i][jj];
+    }
+  };
+  // dlarfg scalars of a step from alpha = top[j][j] and ||x||^2 = F[j][j]
+  // (every thread computes them from the same values); flag: the downdated
+  // norm has cancelled and F must be formed again first.
+  auto scalars = [&](const double alpha, const double xn2, const double nuj, const bool fresh,
+                     double& flag, double& tau_j, double& scale) __attribute__((always_inline)) {
+    flag = 0.0;
+    tau_j = 0.0;
+    scale = 0.0;
+    if (!fresh && nuj > 0.0 && !(xn2 >= kGramTheta * nuj)) {
+      flag = 1.0;
+    } else if (xn2 > 0.0) {
+      const double nrm = sqrt(alpha * alpha + xn2);
+      const double beta = (alpha >= 0.0) ? -nrm : nrm;
+      tau_j = (beta - alpha) / beta;
+      scale = 1.0 / (alpha - beta);
     }
   };
   // After a Gram formation at j0: exports, then the reference norms
   // nu_c = F[c][c] + top[j0][c]^2 (the column's norm^2 over rows >= j0).
+  double s_flag = 0.0, s_tau = 0.0, s_scale = 0.0;   // scalars of the next step
   auto after_form = [&](const int j0) __attribute__((always_inline)) {
-    export_step(j0, j0 & 1, true);
+    export_step(j0, j0 & 1);
     __syncthreads();
-    if (bi == bj) {
+    scalars(L.top[j0][j0], L.ujv[j0 & 1][j0], 0.0, true, s_flag, s_tau, s_scale);
 #pragma unroll
-      for (int i = 0; i < BS; ++i) {
-        const int c = BS * bj + i;
-        L.nu[c] = Fr[i][i] + L.top[j0][c] * L.top[j0][c];
+    for (int i = 0; i < BR; ++i)
+#pragma unroll
+      for (int jj = 0; jj < BC; ++jj) {
+        const int r = BR * bi + i, c = BC * bj + jj;
+        if (r == c) L.nu[c] = Fr[i][jj] + L.top[j0][c] * L.top[j0][c];
       }
-    }
     __syncthreads();
   };
 
@@ -318,12 +329,16 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
   int j = 0;
   while (j < b) {
     const int p = j & 1;
-    if (L.scal[p][0] != 0.0) {
+    if (s_flag != 0.0) {
       form_gram(j, false);
       after_form(j);
       continue;
     }
-    const double tau_j = L.scal[p][1], scale = L.scal[p][2];
+    const double tau_j = s_tau, scale = s_scale;
+    // The next pivot before this step: F[j+1][j+1] and top[j+1][j+1] (row
+    // j + 1 is not written before the barrier below).
+    const double fd1 = L.fdiag[p];
+    const double td1 = (j + 1 < b) ? L.top[j + 1][j + 1] : 0.0;
     // Per column: c_k = tau w_k scale with w_k = v_j^T y_k (k > j), v_p^T v_j
     // (p < j) for T, column j at the top rows below the diagonal, and row
     // j + 1 after this step (removed from F).
@@ -351,6 +366,18 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
       for (int q = 0; q < RPT; ++q) L.xs[g][q] = col[q];
     }
     __syncthreads();
+    // Scalars of step j + 1: its pivot after this step, by the formulas of
+    // the F and top updates below (every thread, from the same values).
+    if (j + 1 < b) {
+      const double fjj0 = L.ujv[p][j];
+      const double c1 = L.cw[j + 1], u1 = L.ujv[p][j + 1], z1 = L.zv[j + 1];
+      double f = fd1 - c1 * u1;
+      f = f - c1 * u1;
+      f = f + (c1 * c1) * fjj0;
+      const double xn2n = f - z1 * z1;
+      const double alphan = td1 - c1 * L.xt[j + 1];
+      scalars(alphan, xn2n, L.nu[j + 1], false, s_flag, s_tau, s_scale);
+    }
     // Apply the step: registers (this workgroup's rows), F and top blocks.
     {
       // Columns k > j lose c_k x_j (c_k = 0 elsewhere).  Column j keeps its
@@ -362,23 +389,23 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
     }
     {
       const double fjj = L.ujv[p][j];
-      double cwc[BS], ujc[BS], zc[BS];
+      double cwc[BC], ujc[BC], zc[BC];
 #pragma unroll
-      for (int jj = 0; jj < BS; ++jj) {
-        const int c = BS * bj + jj;
+      for (int jj = 0; jj < BC; ++jj) {
+        const int c = BC * bj + jj;
         cwc[jj] = L.cw[c];
         ujc[jj] = L.ujv[p][c];
         zc[jj] = L.zv[c];
       }
-      const bool top_rows = (BS * bi + BS - 1 > j) && (BS * bi < b);
+      const bool top_rows = (BR * bi + BR - 1 > j) && (BR * bi < b);
 #pragma unroll
-      for (int i = 0; i < BS; ++i) {
-        const int r = BS * bi + i;
+      for (int i = 0; i < BR; ++i) {
+        const int r = BR * bi + i;
         const double cwr = L.cw[r], ujr = L.ujv[p][r], zr = L.zv[r];
         const double sr = (r == j) ? scale : 1.0;
 #pragma unroll
-        for (int jj = 0; jj < BS; ++jj) {
-          const int c = BS * bj + jj;
+        for (int jj = 0; jj < BC; ++jj) {
+          const int c = BC * bj + jj;
           const double sc = (c == j) ? scale : 1.0;
           double f = Fr[i][jj] - cwc[jj] * ujr;
           f = f - cwr * ujc[jj];
@@ -388,13 +415,13 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
       }
       if (top_rows) {
 #pragma unroll
-        for (int i = 0; i < BS; ++i) {
-          const int r = BS * bi + i;
+        for (int i = 0; i < BR; ++i) {
+          const int r = BR * bi + i;
           if (r > j && r < b) {
             const double xr = L.xt[r];
 #pragma unroll
-            for (int jj = 0; jj < BS; ++jj) {
-              const int c = BS * bj + jj;
+            for (int jj = 0; jj < BC; ++jj) {
+              const int c = BC * bj + jj;
               const double tv = L.top[r][c];
               L.top[r][c] = (c == j) ? scale * xr : tv - cwc[jj] * xr;
             }
@@ -402,7 +429,7 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
         }
       }
     }
-    if (j + 1 < b) export_step(j + 1, p ^ 1, false);
+    if (j + 1 < b) export_step(j + 1, p ^ 1);
     __syncthreads();
     ++j;
   }
@@ -444,12 +471,18 @@ __global__ __launch_bounds__(kPanelThreads) void panel_gram_kernel(GramPanelArgs
   }
 }
 
+// Threads per workgroup: 512 at 64 columns (2 x 4 F entries per thread, two
+// wavefronts per SIMD), 256 otherwise.
+template <int BP>
+constexpr int gram_threads() { return BP == 64 ? 512 : 256; }
+
 template <int BP, int RPT>
 hipError_t gram_go(const GramPanelArgs& a, hipStream_t s) {
-  auto fn = panel_gram_kernel<BP, RPT>;
+  constexpr int NT = gram_threads<BP>();
+  auto fn = panel_gram_kernel<BP, RPT, NT>;
   int occ = 0;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-      &occ, reinterpret_cast<const void*>(fn), kPanelThreads, 0);
+      &occ, reinterpret_cast<const void*>(fn), NT, 0);
   if (e != hipSuccess) return e;
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
@@ -459,15 +492,16 @@ hipError_t gram_go(const GramPanelArgs& a, hipStream_t s) {
   GramPanelArgs arg = a;
   void* params[] = {&arg};
   return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(fn), dim3(a.p.G),
-                                    dim3(kPanelThreads), params, 0, s);
+                                    dim3(NT), params, 0, s);
 }
 
 template <int BP>
 hipError_t gram_rpt(const GramPanelArgs& a, int rpt, hipStream_t s) {
-  constexpr int QC = BP * BP / kPanelThreads;
+  constexpr int NT = gram_threads<BP>();
+  constexpr int QC = BP * BP / NT;
   switch (rpt) {
-    case 4: if constexpr (4 % QC == 0 && (kPanelThreads / BP) * 4 >= BP) return gram_go<BP, 4>(a, s); break;
-    case 8: if constexpr (8 % QC == 0 && (kPanelThreads / BP) * 8 >= BP) return gram_go<BP, 8>(a, s); break;
+    case 4: if constexpr (4 % QC == 0 && (NT / BP) * 4 >= BP) return gram_go<BP, 4>(a, s); break;
+    case 8: if constexpr (8 % QC == 0 && (NT / BP) * 8 >= BP) return gram_go<BP, 8>(a, s); break;
     case 16: if constexpr (16 % QC == 0) return gram_go<BP, 16>(a, s); break;
     case 32: return gram_go<BP, 32>(a, s);
     case 64: return gram_go<BP, 64>(a, s);
@@ -480,8 +514,9 @@ hipError_t gram_rpt(const GramPanelArgs& a, int rpt, hipStream_t s) {
 bool gram_panel_shape(int64_t m, int b, int num_cus, PanelShape* out) {
   if (b < 1 || b > kMaxBlock || m < b) return false;
   const int bp = pad16(b);
-  const int gr = kPanelThreads / bp;
-  const int qc = bp * bp / kPanelThreads;
+  const int nt = bp == 64 ? gram_threads<64>() : gram_threads<32>();
+  const int gr = nt / bp;
+  const int qc = bp * bp / nt;
   static const int rpts[] = {4, 8, 16, 32, 64};
   // The smallest rows-per-thread (short Gram sums, short bulk updates) whose
   // grid stays within half the compute units (a smaller grid exchanges
