@@ -44,10 +44,10 @@ struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
-      rowj, st, trace, Zpart2, W2, tsqr, gx;
+      rowj, st, trace, Zpart2, W2, tsqr, gx, tx;
   size_t total() const {
     return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
-           normpart + red + rowj + st + trace + Zpart2 + W2 + tsqr + gx;
+           normpart + red + rowj + st + trace + Zpart2 + W2 + tsqr + gx + tx;
   }
 };
 
@@ -78,6 +78,7 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.red = (size_t)2 * kMaxPanelWGs * 64 * 2 * 8;
   z.rowj = (size_t)2 * 64 * 2 * 8;
   z.gx = (size_t)(kGramPartWords + kGramSumWords) * 8;
+  z.tx = (size_t)(kThinPartWords + kThinSumWords) * 8;
   z.st = sizeof(DevState);
   z.trace = (size_t)2 * std::max<int64_t>(z.kcap, 1) * 8;
   // Look-ahead: Q_i^T applied to the m x b sample (64 columns at most).
@@ -111,7 +112,7 @@ struct rrf_plan {
   int panel_mode;            // kPanelGrid, kPanelTsqr, kPanelGram or kPanelAuto
   double *V, *Tm, *tau, *Ysum;
   double *normpart, *trace_trail_d, *trace_sub_d;
-  unsigned long long *red, *rowj, *gx;
+  unsigned long long *red, *rowj, *gx, *tx;
   DevState* st;
   DevState* st_host;
   int stop_mode, timing, panel_target;
@@ -474,10 +475,14 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
                  launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
                                         (int)b_next, bpn, bi + shn.rows_pad,
                                         p->Ysum, p->sz.ldysum, s));
-      rrf_status rs = apply_wy<double>(p, 1, V + k + k * ldb, ldb, Tm + k * kTLd,
-                                       kTLd, (int)bi, bp, p->Ysum, p->sz.ldysum,
-                                       mp, b_next, RRF_STAGE_PANEL, p->Zpart2, p->W2);
-      if (rs != RRF_OK) return rs;
+      ThinApplyArgs ta{};
+      ta.V = V + k + k * ldb; ta.ldv = ldb;
+      ta.Tm = Tm + k * kTLd; ta.ldt = kTLd; ta.b = (int)bi;
+      ta.Y = p->Ysum; ta.ldy = p->sz.ldysum; ta.mr = mp; ta.ncols = (int)b_next;
+      ta.part = p->tx; ta.sums = p->tx + kThinPartWords;
+      ta.epoch_base = next_epoch(p); ta.st = p->st;
+      RRF_LAUNCH(p, RRF_STAGE_PANEL, 4.0 * mp * bi * b_next, 16.0 * mp * b_next + 8.0 * mp * bi,
+                 launch_thin_apply(ta, p->num_cus, s));
       pan.Y = p->Ysum + bi; pan.ldy = p->sz.ldysum;
       pan.m = mpn; pan.b = (int)b_next;
       pan.V = V + k_next + k_next * ldb; pan.ldv = ldb;
@@ -648,6 +653,18 @@ rrf_status larfb_stage(rrf_plan* p, int trans, const T* V, int64_t ldv,
   if (e == hipSuccess) e = from_plan_type<T>(Tm, ldt, Tw, kTLd, b, b, s);
   if (e != hipSuccess) return hip_fail(e);
   stats_reset(p);
+  if (std::is_same<T, double>::value && trans && n <= 64) {
+    // Thin binary64 X: the one-launch kernel the look-ahead uses.
+    ThinApplyArgs ta{};
+    ta.V = Vw; ta.ldv = ldb; ta.Tm = Tw; ta.ldt = kTLd; ta.b = (int)b;
+    ta.Y = (double*)X; ta.ldy = ldx; ta.mr = m; ta.ncols = (int)n;
+    ta.part = p->tx; ta.sums = p->tx + kThinPartWords;
+    ta.epoch_base = next_epoch(p); ta.st = p->st;
+    e = launch_thin_apply(ta, p->num_cus, s);
+    if (e == hipSuccess) e = read_state(p);
+    if (e != hipSuccess) return hip_fail(e);
+    return p->st_host->barrier_err ? RRF_ERR_INTERNAL : RRF_OK;
+  }
   return apply_wy<T>(p, trans, Vw, ldb, Tw, kTLd, (int)b, bp, X, ldx, m, n,
                      RRF_STAGE_UPDATE);
 }
@@ -761,6 +778,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   RRF_ALLOC(red, p->sz.red);
   RRF_ALLOC(rowj, p->sz.rowj);
   RRF_ALLOC(gx, p->sz.gx);
+  RRF_ALLOC(tx, p->sz.tx);
   RRF_ALLOC(st, p->sz.st);
   RRF_ALLOC(trace_trail_d, p->sz.trace / 2);
   RRF_ALLOC(trace_sub_d, p->sz.trace / 2);
@@ -774,6 +792,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   if (e == hipSuccess) e = hipMemsetAsync(p->red, 0, p->sz.red, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->rowj, 0, p->sz.rowj, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->gx, 0, p->sz.gx, p->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(p->tx, 0, p->sz.tx, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->st, 0, p->sz.st, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->Om, 0, p->sz.Om, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->V, 0, p->sz.V, p->stream);

@@ -160,6 +160,26 @@ struct GramPanelArgs {
 bool gram_panel_shape(int64_t m, int b, int num_cus, PanelShape* out);
 hipError_t launch_panel_gram(const GramPanelArgs& a, const PanelShape& sh, hipStream_t s);
 
+// Y <- Y - V T^T (V^T Y) for a thin Y (mr x ncols, ncols <= 64), binary64,
+// one cooperative launch (reflectors p >= b and columns >= ncols are
+// treated as zero).  part: kMaxThinWGs x 4096 tagged values, sums: 4096;
+// both zeroed once, epoch unique per launch.
+constexpr int kMaxThinWGs = 256;
+constexpr int64_t kThinPartWords = (int64_t)kMaxThinWGs * 4096 * 2;
+constexpr int64_t kThinSumWords = 4096 * 2;
+struct ThinApplyArgs {
+  const double* V; int64_t ldv;
+  const double* Tm; int64_t ldt; int b;
+  double* Y; int64_t ldy;
+  int64_t mr; int ncols;
+  int64_t rows_per_wg;          // set by the launcher
+  unsigned long long* part;
+  unsigned long long* sums;
+  unsigned epoch_base;
+  DevState* st;
+};
+hipError_t launch_thin_apply(ThinApplyArgs a, int num_cus, hipStream_t s);
+
 // Look-ahead: the update (store, sample width qp) and the panel of the next
 // block in one launch; supported when bp == qp == the panel's padded width.
 bool update_panel_supported(int bp, int qp, const PanelShape& sh);

@@ -7,7 +7,8 @@
              Gram matrix with one exchange per sweep, and tall-skinny QR with
              Householder reconstruction);
 * larfb   -- block reflector application against the oracle's reflector-by-
-             reflector application (both directions).
+             reflector application (both directions; binary64 X of at most 64
+             columns takes the one-launch thin kernel of the look-ahead).
 Tolerances for the floating-point stages are relative to the problem scale
 and the panel's conditioning (stated per test).
 """
@@ -115,7 +116,9 @@ def test_panel_qr_hard_panels(monkeypatch, mode, case):
 @pytest.mark.parametrize("dtype", [np.float64, np.float32])
 @pytest.mark.parametrize("trans", [True, False])
 @pytest.mark.parametrize("m,n,b,seed", [(200, 100, 16, 1), (777, 333, 45, 2),
-                                        (4096, 1000, 64, 3), (64, 7, 8, 4)])
+                                        (4096, 1000, 64, 3), (64, 7, 8, 4),
+                                        (16384, 64, 64, 5), (3001, 48, 32, 6),
+                                        (60000, 37, 50, 7)])
 def test_block_reflector_matches_oracle(dtype, trans, m, n, b, seed):
     say(f"larfb dtype={np.dtype(dtype).name} trans={trans} m={m} n={n} b={b}")
     Y = W.random_graded(m, b, np.float64, seed, decay=1e-2)
