@@ -192,6 +192,18 @@ int red_splits(int64_t mr, int64_t n, int num_cus) {
   return (int)std::max<int64_t>(s, 1);
 }
 
+// Row splits of a reduce over few columns (the explicit-Q pass, a general
+// block reflector), where 32 splits leave each workgroup streaming hundreds
+// of rows on its own: up to 64 splits of at least 128 rows, two workgroups
+// per compute unit, within the partial buffer (max_splits); never fewer than
+// the wide-matrix choice.
+int red_splits_narrow(int64_t mr, int64_t n, int num_cus, int64_t max_splits) {
+  const int64_t col_wgs = ceil_div(n, kRedCols);
+  int64_t s = ceil_div(2 * (int64_t)num_cus, std::max<int64_t>(col_wgs, 1));
+  s = std::min<int64_t>({s, 64, max_splits, std::max<int64_t>(1, mr / 128)});
+  return (int)std::max<int64_t>(s, red_splits(mr, n, num_cus));
+}
+
 // ---- timing / statistics --------------------------------------------------
 
 void stats_reset(rrf_plan* p) {
@@ -299,7 +311,8 @@ rrf_status apply_wy(rrf_plan* p, int trans, const double* V, int64_t ldv,
   if (!Zs) Zs = (T*)p->Zpart;
   if (!Ws) Ws = (T*)p->W;
   const double e = (double)sizeof(T);
-  const int sr0 = red_splits(mr, ncols, p->num_cus);
+  const int sr0 = red_splits_narrow(mr, ncols, p->num_cus,
+                                    (int64_t)kMaxRedSplits * p->n_max / ncols);
   ReduceArgs<T> ra{};
   ra.X = X; ra.ldx = ldx; ra.mr = mr; ra.n = ncols;
   ra.V = V; ra.ldv = ldv; ra.bp = bp;
@@ -322,8 +335,14 @@ rrf_status apply_wy(rrf_plan* p, int trans, const double* V, int64_t ldv,
   ua.V = V; ua.ldv = ldv; ua.bp = bp; ua.W = Ws; ua.ldw = bp;
   ua.Om = nullptr; ua.ldo = kOmLd; ua.qp = 0; ua.P = nullptr; ua.ldp = 0;
   ua.split_stride = 0; ua.s0 = 0; ua.normpart = nullptr;
-  const int su0 = upd_splits(mr, ncols, p->num_cus);
-  ua.cols_per_split = round_up(ceil_div(ncols, su0), kUpdChunk);
+  // No sample here, so column splits cost nothing but a reload of the V
+  // rows: about four workgroups per compute unit, 32 columns or more each.
+  {
+    const int64_t row_wgs = std::max<int64_t>(ceil_div(mr, kUpdRows), 1);
+    int64_t su0 = ceil_div(4 * (int64_t)p->num_cus, row_wgs);
+    su0 = std::max<int64_t>(1, std::min<int64_t>({su0, ncols / 32, 64}));
+    ua.cols_per_split = round_up(ceil_div(ncols, su0), kUpdChunk);
+  }
   const int su = (int)ceil_div(ncols, ua.cols_per_split);
   RRF_LAUNCH(p, stage, fl, 2.0 * e * mr * ncols, launch_update<T>(ua, su, p->stream));
   return RRF_OK;
@@ -477,7 +496,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
                                         p->Ysum, p->sz.ldysum, s));
       ThinApplyArgs ta{};
       ta.V = V + k + k * ldb; ta.ldv = ldb;
-      ta.Tm = Tm + k * kTLd; ta.ldt = kTLd; ta.b = (int)bi;
+      ta.Tm = Tm + k * kTLd; ta.ldt = kTLd; ta.b = (int)bi; ta.trans = 1;
       ta.Y = p->Ysum; ta.ldy = p->sz.ldysum; ta.mr = mp; ta.ncols = (int)b_next;
       ta.part = p->tx; ta.sums = p->tx + kThinPartWords;
       ta.epoch_base = next_epoch(p); ta.st = p->st;
@@ -564,6 +583,19 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     for (int i = blk - 1; i >= 0; --i) {
       const int64_t ki = p->block_start[i];
       const int64_t bi = (i + 1 < blk ? p->block_start[i + 1] : k) - ki;
+      if (k - ki <= 64) {
+        // The last block's columns alone: the one-launch thin kernel.
+        ThinApplyArgs ta{};
+        ta.V = V + ki + ki * ldb; ta.ldv = ldb;
+        ta.Tm = Tm + ki * kTLd; ta.ldt = kTLd; ta.b = (int)bi; ta.trans = 0;
+        ta.Y = Qd + ki + ki * ldb; ta.ldy = ldb; ta.mr = m - ki; ta.ncols = (int)(k - ki);
+        ta.part = p->tx; ta.sums = p->tx + kThinPartWords;
+        ta.epoch_base = next_epoch(p); ta.st = p->st;
+        RRF_LAUNCH(p, RRF_STAGE_ORGQR, 4.0 * (m - ki) * bi * (k - ki),
+                   16.0 * (m - ki) * (k - ki) + 8.0 * (m - ki) * bi,
+                   launch_thin_apply(ta, p->num_cus, s));
+        continue;
+      }
       rrf_status rs = apply_wy<double>(p, 0, V + ki + ki * ldb, ldb,
                                        Tm + ki * kTLd, kTLd, (int)bi, pad16(bi),
                                        Qd + ki + ki * ldb, ldb, m - ki, k - ki,
@@ -576,6 +608,12 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   }
   he = hipStreamSynchronize(s);
   if (he != hipSuccess) return hip_fail(he);
+  if (k > 0) {
+    // The thin kernel's grid exchange (last block) reports a wait that ran out.
+    he = read_state(p);
+    if (he != hipSuccess) return hip_fail(he);
+    if (p->st_host->barrier_err) return RRF_ERR_INTERNAL;
+  }
 
   // Trace back to the host.
   if (blk > 0) {
@@ -653,10 +691,11 @@ rrf_status larfb_stage(rrf_plan* p, int trans, const T* V, int64_t ldv,
   if (e == hipSuccess) e = from_plan_type<T>(Tm, ldt, Tw, kTLd, b, b, s);
   if (e != hipSuccess) return hip_fail(e);
   stats_reset(p);
-  if (std::is_same<T, double>::value && trans && n <= 64) {
+  if (std::is_same<T, double>::value && n <= 64) {
     // Thin binary64 X: the one-launch kernel the look-ahead uses.
     ThinApplyArgs ta{};
     ta.V = Vw; ta.ldv = ldb; ta.Tm = Tw; ta.ldt = kTLd; ta.b = (int)b;
+    ta.trans = trans ? 1 : 0;
     ta.Y = (double*)X; ta.ldy = ldx; ta.mr = m; ta.ncols = (int)n;
     ta.part = p->tx; ta.sums = p->tx + kThinPartWords;
     ta.epoch_base = next_epoch(p); ta.st = p->st;

@@ -170,6 +170,7 @@ constexpr int64_t kThinSumWords = 4096 * 2;
 struct ThinApplyArgs {
   const double* V; int64_t ldv;
   const double* Tm; int64_t ldt; int b;
+  int trans;                    // 1: Y <- Q^T Y (W = T^T Z),  0: Y <- Q Y (W = T Z)
   double* Y; int64_t ldy;
   int64_t mr; int ncols;
   int64_t rows_per_wg;          // set by the launcher

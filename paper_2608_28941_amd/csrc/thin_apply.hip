@@ -1,7 +1,8 @@
 // Block reflector applied to a thin matrix in one cooperative launch:
 // Y <- Q^T Y = Y - V T^T (V^T Y) (Alg. 2, update step, Eq. (4)) for Y of at
 // most 64 columns, the look-ahead's redundant panel update Q_i^T S_{i+1}
-// (Sec. 5).  Three phases instead of three launches (reduce, formW, update):
+// (Sec. 5), or Y <- Q Y = Y - V T (V^T Y), the last block of the explicit-Q
+// pass.  Three phases instead of three launches (reduce, formW, update):
 //   1. every workgroup forms the partial Z_w = V_w^T Y_w of its rows with f64
 //      MFMA (16 x 16 tiles, the output layout kept so that the tagged words
 //      are coalesced);
@@ -37,14 +38,24 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
   const int64_t r_end = min(a.mr, r_begin + a.rows_per_wg);
   const unsigned epoch = a.epoch_base + 1u;
 
-  // T (leading b x b block, upper triangular) to LDS; unconditional loads
-  // (all in flight together), masked by multiplication.
+  // T (leading b x b block, upper triangular) to LDS: all loads issued
+  // before the first use (columns past b read column 0), entries outside the
+  // triangle replaced by zero (a select: whatever the padding holds, even a
+  // NaN, does not reach W).
+  {
+    double tv[16];
 #pragma unroll
-  for (int it = 0; it < 16; ++it) {
-    const int idx = t + 256 * it;
-    const int i = idx % 64, j = idx / 64;
-    const double msk = (i <= j && j < a.b) ? 1.0 : 0.0;
-    Tl[i][j] = msk * a.Tm[i + (int64_t)j * a.ldt];
+    for (int it = 0; it < 16; ++it) {
+      const int idx = t + 256 * it;
+      const int i = idx % 64, j = idx / 64;
+      tv[it] = a.Tm[i + (int64_t)(j < a.b ? j : 0) * a.ldt];
+    }
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const int idx = t + 256 * it;
+      const int i = idx % 64, j = idx / 64;
+      Tl[i][j] = (i <= j && j < a.b) ? tv[it] : 0.0;
+    }
   }
   // Rows [r0, r0 + 64) of V (reflectors < b) and Y (columns < ncols) to LDS,
   // zero elsewhere: thread t loads row t % 64 of 16 columns, so every
@@ -164,16 +175,17 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
     }
   }
   __syncthreads();
-  // W = T^T Z (T is zero outside its upper b x b triangle) with MFMA:
-  // tile (pt = wave, ct), A[m][k] = T[l][16 pt + m], B[k][n] = Z[l][16 ct + n],
-  // into registers, then over Z.
+  // W = T^T Z or T Z (T is zero outside its upper b x b triangle) with MFMA:
+  // tile (pt = wave, ct), A[m][k] = T[k][16 pt + m] (or T[16 pt + m][k]),
+  // B[k][n] = Z[k][16 ct + n], into registers, then over Z.
   {
     d4_t wacc[4];
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) wacc[ct] = d4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
     for (int s4 = 0; s4 < 16; ++s4) {
-      const double av = Tl[4 * s4 + l16][16 * wv + m16];
+      const double av = a.trans ? Tl[4 * s4 + l16][16 * wv + m16]
+                                : Tl[16 * wv + m16][4 * s4 + l16];
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct)
         wacc[ct] = Mfma<double>::op(av, ZW[4 * s4 + l16][16 * ct + m16], wacc[ct]);

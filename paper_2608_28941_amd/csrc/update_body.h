@@ -114,13 +114,12 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
   for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) pacc[rt][qt] = Mfma<T>::zero();
-  double nb = 0.0, nt = 0.0;
-  double wb[RT], wt[RT];   // block-row or trailing norm
+  // Squared norms per row tile (one FMA per element: f64 VALU work takes
+  // issue slots from the MFMA); a lane's rows of one tile fall either in the
+  // block rows (< s0) or in the trailing rows, split after the sweep.
+  double nq[RT];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    wb[rt] = r[rt] < a.s0 ? 1.0 : 0.0;
-    wt[rt] = 1.0 - wb[rt];
-  }
+  for (int rt = 0; rt < RT; ++rt) nq[rt] = 0.0;
 
   // Byte offsets.  Item i of a tile holds column drow(g, i) = drow(g, 0) +
   // i * dstep; the lane part covers the row and drow(g, 0), the uniform part
@@ -246,8 +245,7 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const double v = (double)t[rt][ct][i];
-          nb = fma(v * wb[rt], v, nb);
-          nt = fma(v * wt[rt], v, nt);
+          nq[rt] = fma(v, v, nq[rt]);
         }
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct)
@@ -282,6 +280,12 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
       }
   }
   if (a.normpart) {
+    double nb = 0.0, nt = 0.0;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      if (r[rt] < a.s0) nb += nq[rt];
+      else nt += nq[rt];
+    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
       nb += __shfl_xor(nb, off);

@@ -171,11 +171,27 @@ __global__ __launch_bounds__(256, 2) void reduce_kernel(ReduceArgs<T> a) {
 template <typename T, int BP>
 __global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
   constexpr int CPB = 256 / BP;
+  constexpr int NT = (BP * BP) / 256;
+  constexpr int ZB = 8;                // split partials loaded together
   __shared__ double Tl[BP][BP + 1];
   __shared__ double zs[CPB][BP + 1];
-  for (int idx = threadIdx.x; idx < BP * BP; idx += 256) {
-    const int i = idx % BP, j = idx / BP;
-    Tl[i][j] = (i <= j && j < a.b) ? a.Tm[i + j * a.ldt] : 0.0;
+  // T to LDS: all loads issued before the first use (in-bounds addresses:
+  // columns past b read column 0), entries outside the upper b x b triangle
+  // replaced by zero.
+  {
+    double tv[NT];
+#pragma unroll
+    for (int it = 0; it < NT; ++it) {
+      const int idx = threadIdx.x + 256 * it;
+      const int i = idx % BP, j = idx / BP;
+      tv[it] = a.Tm[i + (int64_t)(j < a.b ? j : 0) * a.ldt];
+    }
+#pragma unroll
+    for (int it = 0; it < NT; ++it) {
+      const int idx = threadIdx.x + 256 * it;
+      const int i = idx % BP, j = idx / BP;
+      Tl[i][j] = (i <= j && j < a.b) ? tv[it] : 0.0;
+    }
   }
   const int p = threadIdx.x % BP, cl = threadIdx.x / BP;
   // Rows [n, round_up(n, kUpdChunk)) of W are written as zeros so the update
@@ -185,11 +201,20 @@ __global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
        c0 += (int64_t)gridDim.x * CPB) {
     __syncthreads();
     const int64_t c = c0 + cl;
+    // z_c = sum over the splits in split order, ZB loads in flight at a time
+    // (clamped split index, surplus loads not added).
+    const T* zp = a.Z + (c < a.n ? c : 0) * BP + p;
     double z = 0.0;
-    if (c < a.n)
-      for (int s = 0; s < a.nsplit; ++s)
-        z += (double)a.Z[s * a.split_stride + c * BP + p];
-    zs[cl][p] = z;
+    for (int s0 = 0; s0 < a.nsplit; s0 += ZB) {
+      T v[ZB];
+#pragma unroll
+      for (int u = 0; u < ZB; ++u)
+        v[u] = zp[(int64_t)min(s0 + u, a.nsplit - 1) * a.split_stride];
+#pragma unroll
+      for (int u = 0; u < ZB; ++u)
+        if (s0 + u < a.nsplit) z += (double)v[u];
+    }
+    zs[cl][p] = c < a.n ? z : 0.0;
     __syncthreads();
     double w = 0.0;
     if (a.trans) {
