@@ -5,6 +5,8 @@
 
 #pragma once
 
+#include <type_traits>
+
 #include "mfma.h"
 #include "rrf_internal.h"
 
@@ -74,8 +76,12 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
   constexpr int NCT = kUpdChunk / 16;
   constexpr int E = (int)sizeof(T);
   static_assert(kUpdRows == 64 * RT, "workgroup height");
-  __shared__ T wl[kUpdChunk * (BP > 0 ? LDW : 1)];
-  __shared__ T ol[kUpdChunk * (QP > 0 ? LDO : 1)];
+  // Staged W and Omega chunks, double buffered: chunk c is read from buffer
+  // c % 2 while chunk c + 1 is written to the other one, so one barrier per
+  // chunk separates both the reads from the next overwrite and the writes
+  // from the next reads.
+  __shared__ T wl[2][kUpdChunk * (BP > 0 ? LDW : 1)];
+  __shared__ T ol[2][kUpdChunk * (QP > 0 ? LDO : 1)];
   __shared__ double nred[2][4];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -145,10 +151,11 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
   // carry zero rows up to the next multiple and the B loads return zero.
   //
   // Schedule per chunk: issue the next chunk's loads, compute and store this
-  // chunk, then (after a barrier) move the next chunk's staging values into
-  // LDS and its B tiles into the accumulators.  The waits for those loads sit
-  // in straight-line code after the stores, so they never wait for stores
-  // (the vector-memory counter retires in issue order).
+  // chunk, then move the next chunk's staging values into the other LDS
+  // buffer and its B tiles into the accumulators, and meet at the barrier.
+  // The waits for those loads sit in straight-line code after the stores, so
+  // they never wait for stores (the vector-memory counter retires in issue
+  // order).
   constexpr int NW = BP > 0 ? (kUpdChunk * BP) / 256 : 0;
   constexpr int NO = (kUpdChunk * QP) / 256;
   static_assert((kUpdChunk * BP) % 256 == 0 && (kUpdChunk * QP) % 256 == 0,
@@ -188,29 +195,34 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
         for (int i = 0; i < 4; ++i)
           bx[rt][ct][i] = Buf<T>::ld(rs, vs[rt] + ct * tstep_s + i * cstep_s);
   };
-  auto stage_chunk = [&]() {
+  auto stage_chunk = [&](T* wb, T* ob) {
 #pragma unroll
     for (int it = 0; it < NW; ++it) {
       const int idx = threadIdx.x + 256 * it;
-      wl[(idx / BP) * LDW + idx % BP] = tw[it];
+      wb[(idx / BP) * LDW + idx % BP] = tw[it];
     }
 #pragma unroll
     for (int it = 0; it < NO; ++it) {
       const int idx = threadIdx.x + 256 * it;
-      ol[(idx / QP) * LDO + idx % QP] = to[it];
+      ob[(idx / QP) * LDO + idx % QP] = to[it];
     }
   };
 
   acc_t t[RT][NCT];
   load_chunk(cs);
-  stage_chunk();
+  stage_chunk(wl[0], ol[0]);
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct) t[rt][ct] = bx[rt][ct];
   __syncthreads();
 
-  for (int64_t c0 = cs; c0 < ce; c0 += kUpdChunk) {
+  // One chunk from buffer CUR (a compile-time constant: the loop below is
+  // unrolled by two so that both buffers have fixed LDS offsets).
+  auto chunk = [&](const int64_t c0, auto cur_tag) {
+    constexpr int CUR = decltype(cur_tag)::value;
+    const T* wlc = wl[CUR];
+    const T* olc = ol[CUR];
     load_chunk(min(c0 + kUpdChunk, c_last));
 
     // Rank-b update of all tiles first, so that the samples do not wait on
@@ -220,7 +232,7 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
       for (int p4 = 0; p4 < NP4; ++p4) {
-        const T wa = wl[(ct * 16 + m16) * LDW + 4 * p4 + g];
+        const T wa = wlc[(ct * 16 + m16) * LDW + 4 * p4 + g];
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
           t[rt][ct] = Mfma<T>::op(wa, vreg[rt][p4], t[rt][ct]);
@@ -253,18 +265,21 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int qt = 0; qt < NQT; ++qt) {
-          const T oa = ol[(ct * 16 + Mfma<T>::drow(g, s)) * LDO + qt * 16 + m16];
+          const T oa = olc[(ct * 16 + Mfma<T>::drow(g, s)) * LDO + qt * 16 + m16];
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt)
             pacc[rt][qt] = Mfma<T>::op(oa, t[rt][ct][s], pacc[rt][qt]);
         }
-    __syncthreads();
-    stage_chunk();
+    stage_chunk(wl[CUR ^ 1], ol[CUR ^ 1]);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct) t[rt][ct] = bx[rt][ct];
     __syncthreads();
+  };
+  for (int64_t c0 = cs; c0 < ce; c0 += 2 * kUpdChunk) {
+    chunk(c0, std::integral_constant<int, 0>());
+    if (c0 + kUpdChunk < ce) chunk(c0 + kUpdChunk, std::integral_constant<int, 1>());
   }
 
   if (QP > 0) {
