@@ -22,6 +22,8 @@
 //   reduce: a wavefront owns 16 columns and all b reflectors; V rows are
 //           staged in LDS and shared; B is read straight into registers.
 
+#include <type_traits>
+
 #include "mfma.h"
 #include "rrf_internal.h"
 #include "update_body.h"
@@ -61,7 +63,10 @@ __global__ __launch_bounds__(256, 2) void reduce_kernel(ReduceArgs<T> a) {
   static_assert(RC % GR == 0 && kRedChunk % RC == 0 && 256 % RC == 0 &&
                 (BP * RC) % 256 == 0, "chunk shape");
   static_assert(kRedCols == 64 * CT, "workgroup width");
-  __shared__ T vl[BP * LDV];
+  // Staged V rows, double buffered (chunk c in buffer c % 2): one barrier per
+  // chunk orders the reads of a buffer before its next overwrite and the
+  // writes before the next reads.
+  __shared__ T vl[2][BP * LDV];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m16 = lane & 15, g = lane >> 4;
@@ -113,17 +118,21 @@ __global__ __launch_bounds__(256, 2) void reduce_kernel(ReduceArgs<T> a) {
 #pragma unroll
     for (int it = 0; it < NIT; ++it) vt[it] = Vr[(int64_t)(p0 + PSTEP * it) * a.ldv];
   };
-  auto stage_v = [&](int64_t R) {
+  auto stage_v = [&](int64_t R, T* vb) {
     const double mask = R + rr < r_end ? 1.0 : 0.0;
 #pragma unroll
-    for (int it = 0; it < NIT; ++it) vl[(p0 + PSTEP * it) * LDV + rr] = (T)(mask * vt[it]);
+    for (int it = 0; it < NIT; ++it) vb[(p0 + PSTEP * it) * LDV + rr] = (T)(mask * vt[it]);
   };
 
   load_x(r_begin, xcur);
   load_v(r_begin);
-  stage_v(r_begin);
+  stage_v(r_begin, vl[0]);
   __syncthreads();
-  for (int64_t R = r_begin; R < r_end; R += RC) {
+  // One chunk from buffer CUR (a compile-time constant: the loop is unrolled
+  // by two so that both buffers have fixed LDS offsets).
+  auto chunk = [&](const int64_t R, auto cur_tag) {
+    constexpr int CUR = decltype(cur_tag)::value;
+    const T* vc = vl[CUR];
     const int64_t Rn = min(R + RC, R_last);
     load_x(Rn, xnxt);
     load_v(Rn);
@@ -134,20 +143,23 @@ __global__ __launch_bounds__(256, 2) void reduce_kernel(ReduceArgs<T> a) {
         const int k = GR * u + VEC * g + h;
 #pragma unroll
         for (int pt = 0; pt < NPT; ++pt) {
-          const T bv = vl[(pt * 16 + m16) * LDV + k];
+          const T bv = vc[(pt * 16 + m16) * LDV + k];
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct)
             acc[ct][pt] = Mfma<T>::op(xcur[ct][u].v[h], bv, acc[ct][pt]);
         }
       }
     }
-    __syncthreads();
-    stage_v(Rn);
+    stage_v(Rn, vl[CUR ^ 1]);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
       for (int u = 0; u < NX; ++u) xcur[ct][u] = xnxt[ct][u];
     __syncthreads();
+  };
+  for (int64_t R = r_begin; R < r_end; R += 2 * RC) {
+    chunk(R, std::integral_constant<int, 0>());
+    if (R + RC < r_end) chunk(R + RC, std::integral_constant<int, 1>());
   }
   // Lane holds Z^T[c = cb + 16 ct + drow(g, i)][p = pt * 16 + m16].
   T* Z = a.Z + (int64_t)blockIdx.y * a.split_stride;
