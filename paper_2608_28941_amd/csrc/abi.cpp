@@ -422,6 +422,9 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     const int bp = pad16(bi);
     const int64_t mp = m - k;
     p->block_start.push_back(k);
+    const int64_t k_next = k + bi;
+    const int64_t b_next = k_next < kcap ? std::min(b, kcap - k_next) : 0;
+    bool s1_done = false;      // block 0: S_1 = A Omega_1 taken with the panel
     if (panel_ready) {
       panel_ready = false;
     } else {
@@ -437,19 +440,44 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       pa.V = V + k + k * ldb; pa.ldv = ldb;
       pa.Tm = Tm + k * kTLd; pa.ldt = kTLd; pa.tau = tau + k;
       pa.red = p->red; pa.rowj = p->rowj; pa.st = p->st; pa.G = sh.G;
-      RRF_LAUNCH(p, RRF_STAGE_PANEL,
-                 2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi,
-                 16.0 * mp * bi, run_panel(p, pa, sh, s));
+      const double pflops =
+          2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi;
+      const int occ0 = la && blk == 0 && b_next > 0 && pad16(b_next) == 64 &&
+                               panel_alg(p, (int)bi) == kPanelGrid &&
+                               sample_panel_supported(64, sh)
+                           ? sample_panel_occupancy<T>(sh) : 0;
+      if (occ0 > 0 && (int64_t)occ0 * p->num_cus > sh.G) {
+        // Look-ahead, block 0: the panel of block 0 and the first look-ahead
+        // sample S_1 = A Omega_1 (independent of it) in one launch.  The
+        // gather above has already read the partials of Y_0 that S_1 replaces.
+        RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
+                   launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_next, b_next,
+                                    Om, kOmLd, 1, s));
+        UpdateArgs<T> u1 = u;
+        u1.qp = 64;
+        u1.normpart = nullptr;
+        const int su1 = upd_splits_fused(m, n, (int64_t)occ0 * p->num_cus - sh.G);
+        u1.cols_per_split = round_up(ceil_div(n, su1), kUpdChunk);
+        const int ys1 = (int)ceil_div(n, u1.cols_per_split);
+        pa.epoch_base = next_epoch(p);
+        RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 2.0 * m * n * b_next + pflops,
+                   e * (m * n + m * b_next) + 16.0 * mp * bi,
+                   launch_sample_panel<T>(u1, ys1, pa, sh, s));
+        ysplits = ys1;
+        yoff = 0;
+        s1_done = true;
+      } else {
+        RRF_LAUNCH(p, RRF_STAGE_PANEL, pflops, 16.0 * mp * bi, run_panel(p, pa, sh, s));
+      }
     }
 
-    const int64_t k_next = k + bi;
-    const int64_t b_next = k_next < kcap ? std::min(b, kcap - k_next) : 0;
     const T* src = blk == 0 ? A : Bws;
     const int64_t lsrc = blk == 0 ? lda : ldb;
 
-    // Look-ahead, block 0: S_1 = A Omega_1 (later blocks get their look-ahead
-    // sample from the previous update).
-    if (la && blk == 0 && b_next > 0) {
+    // Look-ahead, block 0: S_1 = A Omega_1 if it was not taken with the panel
+    // above (later blocks get their look-ahead sample from the previous
+    // update).
+    if (la && blk == 0 && b_next > 0 && !s1_done) {
       RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
                  launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_next, b_next,
                                   Om, kOmLd, 1, s));

@@ -191,6 +191,15 @@ hipError_t launch_update_panel(const UpdateArgs<T>& ua, int nsplit,
 // Workgroups of that launch resident per compute unit (0 if unknown).
 template <typename T>
 int update_panel_occupancy(const PanelShape& sh);
+// Block 0: the first look-ahead sample (ua.bp = 0, no store, qp = 64) and the
+// panel of block 0 in one launch; supported for 64-column panels.
+bool sample_panel_supported(int qp, const PanelShape& sh);
+template <typename T>
+hipError_t launch_sample_panel(const UpdateArgs<T>& ua, int nsplit,
+                               const PanelArgs& pa, const PanelShape& sh,
+                               hipStream_t s);
+template <typename T>
+int sample_panel_occupancy(const PanelShape& sh);
 // Ysum[r + k * ldy] = sum_s P_s[r + k * ldp] for r < m, k < b; 0 elsewhere
 // for r < rows_pad, k < bp (binary64).
 template <typename T>
