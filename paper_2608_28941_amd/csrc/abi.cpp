@@ -44,10 +44,10 @@ struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
-      rowj, st, trace, Zpart2, W2, tsqr, gx, tx;
+      rowj, st, trace, tsqr, gx, tx;
   size_t total() const {
     return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
-           normpart + red + rowj + st + trace + Zpart2 + W2 + tsqr + gx + tx;
+           normpart + red + rowj + st + trace + tsqr + gx + tx;
   }
 };
 
@@ -81,9 +81,6 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.tx = (size_t)(kThinPartWords + kThinSumWords) * 8;
   z.st = sizeof(DevState);
   z.trace = (size_t)2 * std::max<int64_t>(z.kcap, 1) * 8;
-  // Look-ahead: Q_i^T applied to the m x b sample (64 columns at most).
-  z.Zpart2 = (size_t)kMaxRedSplits * 64 * 64 * 8;
-  z.W2 = (size_t)(64 + kUpdChunk) * 64 * 8;
   // Tall-skinny QR panel: the largest tree over the block widths the plan
   // allows (the tree shrinks with the panel's rows).
   z.tsqr = 8;
@@ -107,7 +104,6 @@ struct rrf_plan {
   Sizes sz;
   std::vector<void*> dev_allocs;
   void *Bws, *Ypart, *Om, *Zpart, *W, *Q, *Q64;
-  double *Zpart2, *W2;       // scratch of the look-ahead's small reflector application
   double* tsqr;              // scratch of the tall-skinny QR panel
   int panel_mode;            // kPanelGrid, kPanelTsqr, kPanelGram or kPanelAuto
   double *V, *Tm, *tau, *Ysum;
@@ -839,9 +835,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   RRF_ALLOC(Q, p->sz.Q);
   if (p->sz.Q64) RRF_ALLOC(Q64, p->sz.Q64);
   RRF_ALLOC(normpart, p->sz.normpart);
-  RRF_ALLOC(Zpart2, p->sz.Zpart2);
   RRF_ALLOC(tsqr, p->sz.tsqr);
-  RRF_ALLOC(W2, p->sz.W2);
   RRF_ALLOC(red, p->sz.red);
   RRF_ALLOC(rowj, p->sz.rowj);
   RRF_ALLOC(gx, p->sz.gx);
