@@ -98,6 +98,15 @@ def test_scaled_workloads_tsqr_panel(monkeypatch, name, m, n, b, tol):
     _check_against_live_oracle(w, W.build_matrix(w))
 
 
+@pytest.mark.parametrize("name,m,n,b,tol", [SCALED[1], SCALED[2], SCALED[5]])
+def test_scaled_workloads_without_lookahead(monkeypatch, name, m, n, b, tol):
+    # Same bar with the look-ahead off (b = 64 and 48: every panel in its own
+    # launch, no redundant panel update, no block-0 sample/panel launch).
+    monkeypatch.setenv("RRF_LOOKAHEAD", "0")
+    w = W.scaled(name, m, n, block_b=b, tol=tol)
+    _check_against_live_oracle(w, W.build_matrix(w))
+
+
 @pytest.mark.parametrize("name,m,n,b,tol", SCALED)
 def test_scaled_workloads_gram_panel(monkeypatch, name, m, n, b, tol):
     # Same bar with the Gram-matrix panel (chosen at plan creation).
