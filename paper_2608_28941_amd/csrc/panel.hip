@@ -1,6 +1,6 @@
-// Panel Householder QR with T factor (Alg. 2, geqrt step): the cooperative
-// panel kernel (its workgroup body is in panel_body.h), the gather of the
-// sampled panel and the launchers.
+// Panel Householder QR with T factor (Alg. 2, geqrt step): the panel kernel
+// (a grid of mutually waiting workgroups; the workgroup body is in
+// panel_body.h), the gather of the sampled panel and the launchers.
 
 #include "panel_body.h"
 
@@ -39,8 +39,8 @@ hipError_t panel_go(const PanelArgs& a, hipStream_t s) {
   if (occ < 1 || a.G > occ * cus) return hipErrorCooperativeLaunchTooLarge;
   PanelArgs arg = a;
   void* params[] = {&arg};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(fn),
-                                    dim3(a.G), dim3(kPanelThreads), params, 0, s);
+  return launch_resident(reinterpret_cast<const void*>(fn), dim3(a.G),
+                         dim3(kPanelThreads), params, s);
 }
 
 template <int BP>

@@ -1,12 +1,12 @@
 // Panel Householder QR with T factor (Alg. 2, geqrt step): the body of one
-// workgroup w of the cooperative panel grid (panel_kernel, and the panel part
+// workgroup w of the panel grid (panel_kernel, and the panel part
 // of the look-ahead kernel).
 //
 // Factors the sampled panel Y (m x b, b <= 64) column by column with LAPACK
 // dlarfg / geqr2 semantics and builds the compact WY factor T (Eq. (4)) on the
 // fly by the forward columnwise recursion T[:j, j] = -tau_j T[:j, :j] V^T v_j.
 //
-// Layout: a cooperative grid of G workgroups of 256 threads.  Thread t owns
+// Layout: a grid of G workgroups of 256 threads, all resident at once.  Thread t owns
 // column k = t % BP and row group g = t / BP; workgroup w owns rows
 // [w RW, (w + 1) RW) with RW = (256 / BP) * RPT, and thread (k, g) keeps the
 // RPT rows w RW + g + (256 / BP) q of column k in registers for the whole

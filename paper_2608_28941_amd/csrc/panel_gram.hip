@@ -491,8 +491,8 @@ hipError_t gram_go(const GramPanelArgs& a, hipStream_t s) {
   if (occ < 1 || a.p.G > occ * cus) return hipErrorCooperativeLaunchTooLarge;
   GramPanelArgs arg = a;
   void* params[] = {&arg};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(fn), dim3(a.p.G),
-                                    dim3(NT), params, 0, s);
+  return launch_resident(reinterpret_cast<const void*>(fn), dim3(a.p.G), dim3(NT),
+                         params, s);
 }
 
 template <int BP>

@@ -104,6 +104,21 @@ hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s);
 // Panel: picks rows-per-thread and grid size; returns hipErrorInvalidValue
 // if the panel does not fit the register-resident capacity.
 struct PanelShape { int bp, rpt, G; int64_t rows_pad; };
+
+// Launch of a grid whose workgroups wait on each other through the tagged
+// exchange (xchg.h), so all of them must be resident at once.  The launchers
+// check that the grid fits the kernel's occupancy on every compute unit; an
+// ordinary launch then dispatches the whole grid at once (the stream runs
+// one kernel at a time, as the look-ahead kernel's panel part also relies
+// on).  The cooperative-launch API, which also guarantees it beside other
+// streams' work, cost about 10 us of idle device before and after every
+// launch here.  If other work holds compute units, late workgroups start
+// when it drains; the bounded waits (many seconds) absorb that and report
+// an error beyond it, so a wait never hangs.
+inline hipError_t launch_resident(const void* fn, dim3 grid, dim3 block, void** params,
+                                  hipStream_t s) {
+  return hipLaunchKernel(fn, grid, block, params, 0, s);
+}
 bool panel_shape(int64_t m, int b, int num_cus, int target_wgs, PanelShape* out);
 hipError_t launch_panel(const PanelArgs& a, const PanelShape& sh, hipStream_t s);
 // Panel by tall-skinny QR + Householder reconstruction (tsqr.hip).  Leaves
@@ -161,7 +176,7 @@ bool gram_panel_shape(int64_t m, int b, int num_cus, PanelShape* out);
 hipError_t launch_panel_gram(const GramPanelArgs& a, const PanelShape& sh, hipStream_t s);
 
 // Y <- Y - V T^T (V^T Y) for a thin Y (mr x ncols, ncols <= 64), binary64,
-// one cooperative launch (reflectors p >= b and columns >= ncols are
+// one launch (reflectors p >= b and columns >= ncols are
 // treated as zero).  part: kMaxThinWGs x 4096 tagged values, sums: 4096;
 // both zeroed once, epoch unique per launch.
 constexpr int kMaxThinWGs = 256;

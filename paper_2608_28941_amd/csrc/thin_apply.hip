@@ -1,4 +1,5 @@
-// Block reflector applied to a thin matrix in one cooperative launch:
+// Block reflector applied to a thin matrix in one launch (all workgroups
+// resident, launch_resident):
 // Y <- Q^T Y = Y - V T^T (V^T Y) (Alg. 2, update step, Eq. (4)) for Y of at
 // most 64 columns, the look-ahead's redundant panel update Q_i^T S_{i+1}
 // (Sec. 5), or Y <- Q Y = Y - V T (V^T Y), the last block of the explicit-Q
@@ -236,15 +237,15 @@ hipError_t launch_thin_apply(ThinApplyArgs a, int num_cus, hipStream_t s) {
       &occ, reinterpret_cast<const void*>(thin_apply_kernel), 256, 0);
   if (e != hipSuccess) return e;
   // About 64 rows per workgroup, at most one workgroup per compute unit that
-  // can be resident (cooperative launch).
+  // can be resident (the workgroups wait on each other).
   int64_t G = std::min<int64_t>((int64_t)num_cus * std::max(occ, 1), kMaxThinWGs);
   G = std::max<int64_t>(1, std::min<int64_t>(G, ceil_div(a.mr, 64)));
   a.rows_per_wg = round_up(ceil_div(a.mr, G), 16);
   G = ceil_div(a.mr, a.rows_per_wg);
   if (occ < 1 || G > (int64_t)occ * num_cus) return hipErrorCooperativeLaunchTooLarge;
   void* params[] = {&a};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(thin_apply_kernel),
-                                    dim3((unsigned)G), dim3(256), params, 0, s);
+  return launch_resident(reinterpret_cast<const void*>(thin_apply_kernel),
+                         dim3((unsigned)G), dim3(256), params, s);
 }
 
 }  // namespace rrf
