@@ -121,6 +121,7 @@ struct rrf_plan {
   double ms[RRF_NUM_STAGES], flops[RRF_NUM_STAGES], bytes[RRF_NUM_STAGES];
   int64_t launches[RRF_NUM_STAGES];
   std::vector<hipEvent_t> events;
+  hipEvent_t state_ev = nullptr;   // the run state's copy to the host has landed
   std::vector<int> event_stage;
   size_t events_used;
 };
@@ -148,6 +149,7 @@ void free_plan(rrf_plan* p) {
   p->dev_allocs.clear();
   if (p->st_host) (void)hipHostFree(p->st_host);
   for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
+  if (p->state_ev) (void)hipEventDestroy(p->state_ev);
   delete p;
 }
 
@@ -586,12 +588,50 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
                launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
                                p->trace_sub_d, blk, k_next, kcap, mode, tol, 0, s));
-    he = read_state(p);
+    // Without look-ahead the next block's panel depends only on the sample
+    // this update took, not on the stop test: it is queued behind the copy
+    // of the run state, and the host waits for the copy alone, so the device
+    // factors the panel while the host reads the test (if the run stops
+    // here, those reflectors lie past k and are never used).
+    bool next_panel = false;
+    PanelShape shn{};
+    if (!la && b_next > 0 && panel_fits(p, m - k_next, (int)b_next, &shn)) {
+      if (!p->state_ev) {
+        he = hipEventCreateWithFlags(&p->state_ev, hipEventDisableTiming);
+        if (he != hipSuccess) return hip_fail(he);
+      }
+      next_panel = true;
+    }
+    he = hipMemcpyAsync(p->st_host, p->st, sizeof(DevState), hipMemcpyDeviceToHost, s);
+    if (he != hipSuccess) return hip_fail(he);
+    if (next_panel) {
+      he = hipEventRecord(p->state_ev, s);
+      if (he != hipSuccess) return hip_fail(he);
+      const int64_t mpn = m - k_next;
+      RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mpn * b_next * su + 8.0 * mpn * b_next,
+                 launch_gather_panel<T>(Yp + bi, ldb, ldb * 64, su, mpn, (int)b_next,
+                                        pad16(b_next), shn.rows_pad, p->Ysum,
+                                        p->sz.ldysum, s));
+      PanelArgs pn{};
+      pn.Y = p->Ysum; pn.ldy = p->sz.ldysum;
+      pn.m = mpn; pn.b = (int)b_next;
+      pn.V = V + k_next + k_next * ldb; pn.ldv = ldb;
+      pn.Tm = Tm + k_next * kTLd; pn.ldt = kTLd; pn.tau = tau + k_next;
+      pn.red = p->red; pn.rowj = p->rowj; pn.st = p->st; pn.G = shn.G;
+      RRF_LAUNCH(p, RRF_STAGE_PANEL,
+                 2.0 * mpn * b_next * b_next - 2.0 / 3.0 * b_next * b_next * b_next +
+                     1.0 * mpn * b_next * b_next,
+                 16.0 * mpn * b_next, run_panel(p, pn, shn, s));
+      he = hipEventSynchronize(p->state_ev);
+    } else {
+      he = hipStreamSynchronize(s);
+    }
     if (he != hipSuccess) return hip_fail(he);
     k = k_next;
     ++blk;
     yoff = bi;
     ysplits = su;
+    if (next_panel) panel_ready = true;
     if (p->st_host->barrier_err) return RRF_ERR_INTERNAL;
     if (p->st_host->nonfinite) return RRF_ERR_NONFINITE;
     stop = p->st_host->stop != 0;
