@@ -415,6 +415,32 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   int blk = 0;
   bool panel_ready = false;  // the panel of this block was factored by the last update
   bool stop = p->st_host->stop != 0;
+  bool w_ready = false;      // W of this block was formed at the end of the last one
+  double E_prev2 = 0.0;      // the stopping quantity one state read earlier
+
+  // Z = V^T B[kk:m, :] and W = T^T Z of the block at kk (width bb), from the
+  // rows kk..m of sx.
+  auto issue_w = [&](int64_t kk, int64_t bb, const T* sx, int64_t ldsx) -> rrf_status {
+    const int64_t mpp = m - kk;
+    const int bpp = pad16(bb);
+    const int sr0 = red_splits(mpp, n, p->num_cus);
+    ReduceArgs<T> ra{};
+    ra.X = sx + kk; ra.ldx = ldsx; ra.mr = mpp; ra.n = n;
+    ra.V = V + kk + kk * ldb; ra.ldv = ldb; ra.bp = bpp;
+    ra.Z = (T*)p->Zpart; ra.split_stride = n * bpp;
+    ra.rows_per_split = round_up(ceil_div(mpp, sr0), kRedChunk);
+    const int sr = (int)ceil_div(mpp, ra.rows_per_split);
+    RRF_LAUNCH(p, RRF_STAGE_REDUCE, 2.0 * mpp * n * bb, e * mpp * n,
+               launch_reduce<T>(ra, sr, s));
+    FormWArgs<T> fa{};
+    fa.Z = (T*)p->Zpart; fa.nsplit = sr; fa.split_stride = ra.split_stride;
+    fa.Tm = Tm + kk * kTLd; fa.ldt = kTLd; fa.W = (T*)p->W; fa.n = n; fa.bp = bpp;
+    fa.trans = 1;
+    fa.b = (int)bb;
+    RRF_LAUNCH(p, RRF_STAGE_FORMW, 1.0 * n * bb * bb, e * n * bb * (sr + 1),
+               launch_formw<T>(fa, s));
+    return RRF_OK;
+  };
   while (!stop) {
     const int64_t bi = std::min(b, kcap - k);
     const int bp = pad16(bi);
@@ -487,23 +513,14 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       yoff = 0;
     }
 
-    // Z = V_i^T B[k:m, :], W = T_i^T Z.
-    const int sr0 = red_splits(mp, n, p->num_cus);
-    ReduceArgs<T> ra{};
-    ra.X = src + k; ra.ldx = lsrc; ra.mr = mp; ra.n = n;
-    ra.V = V + k + k * ldb; ra.ldv = ldb; ra.bp = bp;
-    ra.Z = (T*)p->Zpart; ra.split_stride = n * bp;
-    ra.rows_per_split = round_up(ceil_div(mp, sr0), kRedChunk);
-    const int sr = (int)ceil_div(mp, ra.rows_per_split);
-    RRF_LAUNCH(p, RRF_STAGE_REDUCE, 2.0 * mp * n * bi, e * mp * n,
-               launch_reduce<T>(ra, sr, s));
-    FormWArgs<T> fa{};
-    fa.Z = (T*)p->Zpart; fa.nsplit = sr; fa.split_stride = ra.split_stride;
-    fa.Tm = Tm + k * kTLd; fa.ldt = kTLd; fa.W = (T*)p->W; fa.n = n; fa.bp = bp;
-    fa.trans = 1;
-    fa.b = (int)bi;
-    RRF_LAUNCH(p, RRF_STAGE_FORMW, 1.0 * n * bi * bi, e * n * bi * (sr + 1),
-               launch_formw<T>(fa, s));
+    // Z = V_i^T B[k:m, :], W = T_i^T Z (unless queued at the end of the last
+    // block).
+    if (w_ready) {
+      w_ready = false;
+    } else {
+      rrf_status rs = issue_w(k, bi, src, lsrc);
+      if (rs != RRF_OK) return rs;
+    }
 
     PanelArgs pan{};          // look-ahead panel of block i + 1
     PanelShape pan_shape{};
@@ -593,20 +610,35 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     // of the run state, and the host waits for the copy alone, so the device
     // factors the panel while the host reads the test (if the run stops
     // here, those reflectors lie past k and are never used).
-    bool next_panel = false;
+    // With look-ahead the next block's panel is already factored, and its W
+    // is queued the same way when the error, extrapolated geometrically from
+    // the last two state reads, stays above sigma^2 after this block: a
+    // wrong guess (the run stops here after all) wastes one reduce.
+    bool next_panel = false, next_w = false;
     PanelShape shn{};
-    if (!la && b_next > 0 && panel_fits(p, m - k_next, (int)b_next, &shn)) {
-      if (!p->state_ev) {
-        he = hipEventCreateWithFlags(&p->state_ev, hipEventDisableTiming);
-        if (he != hipSuccess) return hip_fail(he);
-      }
-      next_panel = true;
+    if (!la && b_next > 0 && panel_fits(p, m - k_next, (int)b_next, &shn)) next_panel = true;
+    if (la && b_next > 0 && panel_ready) {
+      const double E_prev = mode ? p->st_host->E_sub : p->st_host->E_trail;
+      const double E_pred =
+          E_prev2 > 0.0 ? E_prev * std::min(1.0, E_prev / E_prev2) : E_prev;
+      next_w = E_pred > p->st_host->sigma2;
+      E_prev2 = E_prev;
+    }
+    if ((next_panel || next_w) && !p->state_ev) {
+      he = hipEventCreateWithFlags(&p->state_ev, hipEventDisableTiming);
+      if (he != hipSuccess) return hip_fail(he);
     }
     he = hipMemcpyAsync(p->st_host, p->st, sizeof(DevState), hipMemcpyDeviceToHost, s);
     if (he != hipSuccess) return hip_fail(he);
-    if (next_panel) {
+    if (next_panel || next_w) {
       he = hipEventRecord(p->state_ev, s);
       if (he != hipSuccess) return hip_fail(he);
+    }
+    if (next_w) {
+      rrf_status rs = issue_w(k_next, b_next, Bws, ldb);
+      if (rs != RRF_OK) return rs;
+    }
+    if (next_panel) {
       const int64_t mpn = m - k_next;
       RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mpn * b_next * su + 8.0 * mpn * b_next,
                  launch_gather_panel<T>(Yp + bi, ldb, ldb * 64, su, mpn, (int)b_next,
@@ -622,16 +654,15 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
                  2.0 * mpn * b_next * b_next - 2.0 / 3.0 * b_next * b_next * b_next +
                      1.0 * mpn * b_next * b_next,
                  16.0 * mpn * b_next, run_panel(p, pn, shn, s));
-      he = hipEventSynchronize(p->state_ev);
-    } else {
-      he = hipStreamSynchronize(s);
     }
+    he = (next_panel || next_w) ? hipEventSynchronize(p->state_ev) : hipStreamSynchronize(s);
     if (he != hipSuccess) return hip_fail(he);
     k = k_next;
     ++blk;
     yoff = bi;
     ysplits = su;
     if (next_panel) panel_ready = true;
+    if (next_w) w_ready = true;
     if (p->st_host->barrier_err) return RRF_ERR_INTERNAL;
     if (p->st_host->nonfinite) return RRF_ERR_NONFINITE;
     stop = p->st_host->stop != 0;
