@@ -82,6 +82,11 @@ typedef enum rrf_stage {
  *   k_max        rank cap (>= 0); 0 means min(m, n).  A cap below the rank the
  *                tolerance needs is the fixed-rank mode of Sec. 6 (Fig. 6).
  *   hip_stream   hipStream_t to enqueue on; NULL means the null stream.
+ *                Some kernels of a run (the panels, the thin block reflector)
+ *                have workgroups that wait on each other and are launched no
+ *                larger than the device holds at once; work on other streams
+ *                that occupies the device delays them (their waits are
+ *                bounded: RRF_ERR_INTERNAL if one runs out).
  * Returns RRF_ERR_SHAPE if m_max exceeds the register-resident panel capacity
  * (65536 rows for b = 64, 131072 for b = 32, 262144 for b = 16 on 256 CUs),
  * RRF_ERR_HIP if there is no usable GPU, RRF_ERR_NOMEM on allocation failure.
