@@ -53,6 +53,8 @@ def parse():
                     help="extra runs with per-kernel HIP-event timing")
     ap.add_argument("--fixed-rank", default=None, metavar="R[,R..]",
                     help="only the fixed-rank comparison at these ranks")
+    ap.add_argument("--subspace-map", action="store_true",
+                    help="only time the GaLore subspace map (Sec. 7) on galore-sized bases")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run one device-to-device copy of MIB MiB")
     ap.add_argument("--summarize", nargs="+", default=None, metavar="DIR",
@@ -306,6 +308,37 @@ def fixed_rank(a):
                       "steps": a.steps, "results": out}))
 
 
+def subspace_map_bench(a):
+    """Time rrf_subspace_map (Q_new^T (Q_old M)) for the galore_fp32_4096x4096
+    shape: 4096-row fp32 bases of ranks 512 and 448 and a 512 x 4096 state,
+    random orthonormal bases (synthetic)."""
+    import torch
+    import paper_2608_28941_amd as rrf
+    m, r0, r1, n = 4096, 512, 448, 4096
+    g = torch.Generator(device="cpu").manual_seed(9)
+    Q_old = torch.linalg.qr(torch.randn(m, r0, generator=g, dtype=torch.float64))[0]
+    Q_new = torch.linalg.qr(torch.randn(m, r1, generator=g, dtype=torch.float64))[0]
+    M = torch.randn(r0, n, generator=g, dtype=torch.float64)
+    dev = [rrf.colmajor(t.to(torch.float32).to("cuda:0")) for t in (Q_new, Q_old, M)]
+    with rrf.Plan(torch.float32, m, n, 64) as p:
+        for _ in range(max(a.warmup, 1)):
+            p.subspace_map(*dev)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(a.steps):
+            out = p.subspace_map(*dev)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / a.steps
+    flops = 2.0 * m * r1 * r0 + 2.0 * r1 * r0 * n
+    ref = Q_new.T @ (Q_old @ M)
+    err = float((out.double().cpu() - ref).abs().max())
+    print(json.dumps({"op": "subspace_map", "m": m, "r_old": r0, "r_new": r1, "n": n,
+                      "dtype": "f32", "ms": round(dt * 1e3, 4),
+                      "tflops": round(flops / dt / 1e12, 2),
+                      "frac_of_fp32_mfma_peak": round(flops / dt / 1e12 / PEAK_TFLOPS["float32"], 3),
+                      "max_abs_err_vs_fp64": err, "data": "synthetic"}))
+
+
 def copy_probe(mib):
     """One device copy of ``mib`` MiB through the library's copy kernel:
     reads and writes exactly mib MiB, the scale for FETCH_SIZE/WRITE_SIZE."""
@@ -387,6 +420,9 @@ def main():
         sys.exit(2)
     if a.copy_probe > 0:
         copy_probe(a.copy_probe)
+        return
+    if a.subspace_map:
+        subspace_map_bench(a)
         return
     if a.fixed_rank:
         fixed_rank(a)

@@ -17,6 +17,8 @@ Based on an Implicit Householder QR Decomposition"):
 * ``stability``   -- the Sec. 6 stability experiment (Fig. 3) in fp32:
                      Alg. 2 against block Gram-Schmidt (Alg. 1) with and
                      without reorthogonalisation (``python -m oracle.stability``).
+* ``subspace_map`` -- the GaLore subspace-consistency map of Sec. 7,
+                     Q_{t+1}^T Q_t M_t, in float64.
 
 Every function cites the passage it follows.  Pins against independent facts
 (LAPACK, SVD, closed forms, invariants) live in ``tests/test_oracle_*.py``.
@@ -33,6 +35,7 @@ from .range_finder import (
     org2r,
     frob2,
 )
+from .subspace import subspace_map
 
 __all__ = [
     "normal_v1",
@@ -45,4 +48,5 @@ __all__ = [
     "larft",
     "org2r",
     "frob2",
+    "subspace_map",
 ]

@@ -53,7 +53,7 @@ def colmajor(t):
 def _check_colmajor(t, name):
     if t.dim() != 2 or not t.is_cuda:
         raise ValueError(f"{name} must be a 2-D CUDA tensor")
-    if t.shape[0] > 1 and t.stride(0) != 1:
+    if t.numel() > 0 and t.shape[0] > 1 and t.stride(0) != 1:
         raise ValueError(f"{name} must be column-major (use colmajor())")
     return max(1, t.stride(1) if t.shape[1] > 1 else t.shape[0])
 
@@ -221,6 +221,26 @@ class Plan:
             ctypes.c_void_p(T.data_ptr()), ldt, b, ctypes.c_void_p(X.data_ptr()),
             X.shape[0], X.shape[1], ldx), "rrf_apply_block_reflector")
         return X
+
+    def subspace_map(self, Q_new, Q_old, M):
+        """GaLore subspace map: Q_new^T (Q_old M) as a new column-major tensor."""
+        for t, name in ((Q_new, "Q_new"), (Q_old, "Q_old"), (M, "M")):
+            if t.dtype != self.dtype:
+                raise TypeError(f"{name}'s dtype differs from the plan's")
+        ldqn = _check_colmajor(Q_new, "Q_new")
+        ldqo = _check_colmajor(Q_old, "Q_old")
+        ldm = _check_colmajor(M, "M")
+        m, r_new = Q_new.shape
+        if Q_old.shape[0] != m or M.shape[0] != Q_old.shape[1]:
+            raise ValueError("shapes do not chain: Q_new m x r1, Q_old m x r0, M r0 x n")
+        r_old, n = Q_old.shape[1], M.shape[1]
+        out = _alloc_colmajor(r_new, n, max(r_new, 1), self.dtype, self.device)
+        _abi.check(self.lib.rrf_subspace_map(
+            self.handle, ctypes.c_void_p(Q_new.data_ptr()), ldqn, r_new,
+            ctypes.c_void_p(Q_old.data_ptr()), ldqo, r_old,
+            ctypes.c_void_p(M.data_ptr()), ldm, m, n,
+            ctypes.c_void_p(out.data_ptr()), max(r_new, 1)), "rrf_subspace_map")
+        return out
 
 
 def run(A, tol, block_b, seed, k_max=0, stop_mode=RRF_STOP_TRAILING):

@@ -4,7 +4,8 @@
 
 Every source is compiled with hipcc for gfx950 with packed FP32 instructions
 disabled; the sketch generator is also compiled without FP contraction (its
-results must be bit-reproducible from the definition).
+results must be bit-reproducible from the definition).  The library links
+rocBLAS for the two dense GEMMs of the subspace map.
 """
 
 import concurrent.futures as cf
@@ -55,7 +56,8 @@ def build(verbose=False, jobs=None):
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(lambda s: _compile(hipcc, s, verbose), SOURCES))
     tmp = LIB + ".tmp"
-    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
+    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs,
+           "-L/opt/rocm/lib", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib", "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -16,6 +16,7 @@
 // block applications costs about 2 sqrt(s) u sqrt(k) in ||Q^T Q - I||_F.
 
 #include <hip/hip_runtime.h>
+#include <rocblas/rocblas.h>
 
 #include <algorithm>
 #include <cmath>
@@ -122,6 +123,9 @@ struct rrf_plan {
   int64_t launches[RRF_NUM_STAGES];
   std::vector<hipEvent_t> events;
   hipEvent_t state_ev = nullptr;   // the run state's copy to the host has landed
+  rocblas_handle blas = nullptr;   // subspace map (created on first use)
+  void* map_c = nullptr;           // its r_new x r_old product
+  size_t map_c_bytes = 0;
   std::vector<int> event_stage;
   size_t events_used;
 };
@@ -150,6 +154,8 @@ void free_plan(rrf_plan* p) {
   if (p->st_host) (void)hipHostFree(p->st_host);
   for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
   if (p->state_ev) (void)hipEventDestroy(p->state_ev);
+  if (p->blas) (void)rocblas_destroy_handle(p->blas);
+  if (p->map_c) (void)hipFree(p->map_c);
   delete p;
 }
 
@@ -1105,6 +1111,77 @@ rrf_status rrf_apply_block_reflector(rrf_plan_t plan, int trans,
                                (const double*)T, ldt, b, (double*)X, m, n, ldx);
   return larfb_stage<float>(plan, trans, (const float*)V, ldv, (const float*)T,
                             ldt, b, (float*)X, m, n, ldx);
+}
+
+rrf_status rrf_subspace_map(rrf_plan_t plan, const void* Qnew, int64_t ldqn,
+                            int64_t r_new, const void* Qold, int64_t ldqo,
+                            int64_t r_old, const void* M, int64_t ldm,
+                            int64_t m, int64_t n, void* out, int64_t ldo) {
+  if (!plan || m < 0 || n < 0 || r_new < 0 || r_old < 0) return RRF_ERR_INVALID_ARG;
+  // A pointer may be null only where its matrix is empty.
+  if ((!Qnew && m * r_new > 0) || (!Qold && m * r_old > 0) || (!M && r_old * n > 0) ||
+      (!out && r_new * n > 0))
+    return RRF_ERR_INVALID_ARG;
+  if (ldqn < std::max<int64_t>(1, m) ||
+      ldqo < std::max<int64_t>(1, m) || ldm < std::max<int64_t>(1, r_old) ||
+      ldo < std::max<int64_t>(1, r_new))
+    return RRF_ERR_INVALID_ARG;
+  const int64_t lim = 2147483647;
+  if (m > lim || n > lim || r_new > lim || r_old > lim || ldqn > lim || ldqo > lim ||
+      ldm > lim || ldo > lim)
+    return RRF_ERR_SHAPE;
+  if (r_new == 0 || n == 0) return RRF_OK;
+  hipStream_t s = plan->stream;
+  const size_t e = plan->dtype == RRF_F64 ? 8 : 4;
+  if (r_old == 0 || m == 0) {
+    hipError_t he = hipMemset2DAsync(out, (size_t)ldo * e, 0, (size_t)r_new * e, (size_t)n, s);
+    return he == hipSuccess ? RRF_OK : hip_fail(he);
+  }
+  if (!plan->blas) {
+    if (rocblas_create_handle(&plan->blas) != rocblas_status_success) {
+      plan->blas = nullptr;
+      return RRF_ERR_HIP;
+    }
+  }
+  if (rocblas_set_stream(plan->blas, s) != rocblas_status_success) return RRF_ERR_HIP;
+  const size_t need = (size_t)r_new * (size_t)r_old * e;
+  if (need > plan->map_c_bytes) {
+    if (plan->map_c) {
+      (void)hipFree(plan->map_c);
+      plan->map_c = nullptr;
+      plan->map_c_bytes = 0;
+    }
+    if (hipMalloc(&plan->map_c, need) != hipSuccess) {
+      plan->map_c = nullptr;
+      return RRF_ERR_NOMEM;
+    }
+    plan->map_c_bytes = need;
+  }
+  const rocblas_int mi = (rocblas_int)m, ni = (rocblas_int)n;
+  const rocblas_int r1 = (rocblas_int)r_new, r0 = (rocblas_int)r_old;
+  rocblas_status bs;
+  if (plan->dtype == RRF_F64) {
+    const double one = 1.0, zero = 0.0;
+    double* C = (double*)plan->map_c;
+    bs = rocblas_dgemm(plan->blas, rocblas_operation_transpose, rocblas_operation_none,
+                       r1, r0, mi, &one, (const double*)Qnew, (rocblas_int)ldqn,
+                       (const double*)Qold, (rocblas_int)ldqo, &zero, C, r1);
+    if (bs == rocblas_status_success)
+      bs = rocblas_dgemm(plan->blas, rocblas_operation_none, rocblas_operation_none,
+                         r1, ni, r0, &one, C, r1, (const double*)M, (rocblas_int)ldm,
+                         &zero, (double*)out, (rocblas_int)ldo);
+  } else {
+    const float one = 1.0f, zero = 0.0f;
+    float* C = (float*)plan->map_c;
+    bs = rocblas_sgemm(plan->blas, rocblas_operation_transpose, rocblas_operation_none,
+                       r1, r0, mi, &one, (const float*)Qnew, (rocblas_int)ldqn,
+                       (const float*)Qold, (rocblas_int)ldqo, &zero, C, r1);
+    if (bs == rocblas_status_success)
+      bs = rocblas_sgemm(plan->blas, rocblas_operation_none, rocblas_operation_none,
+                         r1, ni, r0, &one, C, r1, (const float*)M, (rocblas_int)ldm,
+                         &zero, (float*)out, (rocblas_int)ldo);
+  }
+  return bs == rocblas_status_success ? RRF_OK : RRF_ERR_HIP;
 }
 
 rrf_status rrf_copy_matrix(rrf_dtype dtype, const void* src, int64_t lds,

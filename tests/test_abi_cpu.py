@@ -79,6 +79,8 @@ def test_invalid_arguments_rejected_before_device():
     assert lib.rrf_panel_qr(None, None, 4, 2, 4, None, 4, None, 2, None) == E
     assert lib.rrf_apply_block_reflector(None, 1, None, 4, None, 2, 2, None, 4,
                                          4, 4) == E
+    assert lib.rrf_subspace_map(None, ctypes.c_void_p(8), 4, 2, ctypes.c_void_p(8), 4, 2,
+                                ctypes.c_void_p(8), 2, 4, 3, ctypes.c_void_p(8), 2) == E
 
 
 def test_plan_create_without_gpu_reports_hip_error():
