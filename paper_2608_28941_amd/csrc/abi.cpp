@@ -611,25 +611,25 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
                launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
                                p->trace_sub_d, blk, k_next, kcap, mode, tol, 0, s));
-    // Without look-ahead the next block's panel depends only on the sample
-    // this update took, not on the stop test: it is queued behind the copy
-    // of the run state, and the host waits for the copy alone, so the device
-    // factors the panel while the host reads the test (if the run stops
-    // here, those reflectors lie past k and are never used).
-    // With look-ahead the next block's panel is already factored, and its W
-    // is queued the same way when the error, extrapolated geometrically from
-    // the last two state reads, stays above sigma^2 after this block: a
-    // wrong guess (the run stops here after all) wastes one reduce.
+    // Work for the next block that does not depend on the stop test is
+    // queued behind the copy of the run state, and the host waits for the
+    // copy alone, so the device keeps working while the host reads the test:
+    // without look-ahead the next block's gather and panel (they need only
+    // the sample this update took), with look-ahead (the next panel is
+    // already factored) its reduce and formW.  It is queued when the
+    // stopping quantity, extrapolated geometrically from the last two state
+    // reads, stays above sigma^2 after this block; a wrong guess (the run
+    // stops here after all) wastes that work, whose results lie past k and
+    // are never used.
+    const double E_prev = mode ? p->st_host->E_sub : p->st_host->E_trail;
+    const double E_pred =
+        E_prev2 > 0.0 ? E_prev * std::min(1.0, E_prev / E_prev2) : E_prev;
+    E_prev2 = E_prev;
+    const bool more_likely = b_next > 0 && E_pred > p->st_host->sigma2;
     bool next_panel = false, next_w = false;
     PanelShape shn{};
-    if (!la && b_next > 0 && panel_fits(p, m - k_next, (int)b_next, &shn)) next_panel = true;
-    if (la && b_next > 0 && panel_ready) {
-      const double E_prev = mode ? p->st_host->E_sub : p->st_host->E_trail;
-      const double E_pred =
-          E_prev2 > 0.0 ? E_prev * std::min(1.0, E_prev / E_prev2) : E_prev;
-      next_w = E_pred > p->st_host->sigma2;
-      E_prev2 = E_prev;
-    }
+    if (!la && more_likely && panel_fits(p, m - k_next, (int)b_next, &shn)) next_panel = true;
+    if (la && more_likely && panel_ready) next_w = true;
     if ((next_panel || next_w) && !p->state_ev) {
       he = hipEventCreateWithFlags(&p->state_ev, hipEventDisableTiming);
       if (he != hipSuccess) return hip_fail(he);
