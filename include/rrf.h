@@ -24,7 +24,9 @@
  *   - A plan is not thread-safe: one plan per host thread / stream.
  *   - Work is enqueued on the plan's HIP stream (or the given stream).
  *     rrf_run synchronises that stream before it returns (k is an output
- *     shape); the stage entry points do not.
+ *     shape); so do rrf_panel_qr and the one-launch form of
+ *     rrf_apply_block_reflector (they read back whether a grid-wide wait
+ *     gave up); the other entry points do not.
  */
 #ifndef RRF_H
 #define RRF_H
@@ -78,7 +80,11 @@ typedef enum rrf_stage {
  * rrf_plan_create -- allocate a plan and its device workspace.
  *   dtype        RRF_F32 or RRF_F64.
  *   m_max,n_max  largest A the plan will see (>= 1).
- *   block_b_max  largest block size b, 1 <= block_b_max <= 64.
+ *   block_b_max  largest block size b, 1 <= block_b_max <= 128.  A block wider
+ *                than 64 columns runs as sub-blocks of 64 (the last one
+ *                ragged): Householder QR is column by column, so the
+ *                reflectors are the block's own; the stop test runs once per
+ *                block.
  *   k_max        rank cap (>= 0); 0 means min(m, n).  A cap below the rank the
  *                tolerance needs is the fixed-rank mode of Sec. 6 (Fig. 6).
  *   hip_stream   hipStream_t to enqueue on; NULL means the null stream.
@@ -87,9 +93,12 @@ typedef enum rrf_stage {
  *                larger than the device holds at once; work on other streams
  *                that occupies the device delays them (their waits are
  *                bounded: RRF_ERR_INTERNAL if one runs out).
- * Returns RRF_ERR_SHAPE if m_max exceeds the register-resident panel capacity
- * (65536 rows for b = 64, 131072 for b = 32, 262144 for b = 16 on 256 CUs),
- * RRF_ERR_HIP if there is no usable GPU, RRF_ERR_NOMEM on allocation failure.
+ * Panels taller than the register-resident panel grid holds (65536 rows for
+ * 64 columns, 131072 for 32, 262144 for 16 on 256 CUs) are factored by a
+ * tall-skinny QR tree instead (no look-ahead for them).
+ * Returns RRF_ERR_SHAPE if m_max exceeds even that tree (about 4 million rows
+ * at 64 columns), RRF_ERR_HIP if there is no usable GPU, RRF_ERR_NOMEM on
+ * allocation failure.
  * On success *plan owns all memory; free it with rrf_destroy.
  * ------------------------------------------------------------------------- */
 rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
@@ -113,7 +122,8 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
  *             min(m, n, k_max)) whose basis meets the tolerance.
  *   *B, *ldb  B = Q^T A, k x n (the top k rows of the in-place workspace).
  * Returns RRF_OK, RRF_WARN_KMAX (cap reached, outputs valid), or an error:
- * RRF_ERR_NONFINITE if A holds NaN/Inf, RRF_ERR_SHAPE if m/n exceed the plan.
+ * RRF_ERR_NONFINITE if A holds NaN/Inf, RRF_ERR_SHAPE if m/n exceed the plan,
+ * RRF_ERR_INTERNAL if a grid-wide wait gave up (outputs undefined).
  * ------------------------------------------------------------------------- */
 rrf_status rrf_run(rrf_plan_t plan, const void* A, int64_t m, int64_t n,
                    int64_t lda, double tol, int64_t block_b, uint64_t seed,
@@ -147,7 +157,10 @@ rrf_status rrf_get_trace(rrf_plan_t plan, int64_t cap, int64_t* nblocks,
 /* Per-stage statistics of the last run, host arrays of length RRF_NUM_STAGES:
  * ms[s]       summed kernel time (HIP events; 0 unless timing was enabled),
  * launches[s] kernel launches, flops[s] algorithmic flops, bytes[s]
- * algorithmic HBM bytes (each operand read or written once per kernel). */
+ * algorithmic HBM bytes (each operand read or written once per kernel).
+ * Work queued ahead of a stop test for a sub-block past the final k (a
+ * look-ahead sample, panel or W that the method never used) is not counted
+ * in flops and bytes; its time is in ms. */
 rrf_status rrf_get_stage_stats(rrf_plan_t plan, double* ms, int64_t* launches,
                                double* flops, double* bytes);
 
@@ -155,8 +168,9 @@ rrf_status rrf_get_stage_stats(rrf_plan_t plan, double* ms, int64_t* launches,
  * binary64 (double) for both dtypes -- the panel factorisation runs in
  * binary64 and float plans round V only when they apply it:
  * V (m x k, unit lower trapezoidal, explicit ones and zeros, ldv),
- * T (block i's upper triangular T_i in rows 0..b_i-1 of columns
- * [i b, i b + b_i), like LAPACK geqrt's T; ldt), tau (k).
+ * T (the upper triangular T of each sub-block of at most 64 columns in rows
+ * 0..w-1 of the sub-block's w columns, like LAPACK geqrt's T with nb = 64;
+ * for block_b <= 64 the sub-blocks are the blocks; ldt), tau (k).
  * A stage entry point called after the run overwrites them. */
 rrf_status rrf_get_reflectors(rrf_plan_t plan, const void** V, int64_t* ldv,
                               const void** T, int64_t* ldt, const void** tau);
@@ -177,7 +191,10 @@ rrf_status rrf_sketch(rrf_dtype dtype, uint64_t seed, int64_t n, int64_t col0,
  * semantics, dlarfg sign convention).  Y: m x b (ldy), read only.
  * Outputs: V (m x b, ldv >= m, unit lower trapezoidal with explicit ones and
  * zeros), T (b x b upper triangular, ldt >= b, lower part zeroed), tau (b).
- * Requires 1 <= b <= plan's block_b_max, b <= m <= plan's m_max. */
+ * Requires 1 <= b <= min(plan's block_b_max, 64), b <= m <= plan's m_max.
+ * Panels taller than the register-resident grid holds take the tall-skinny
+ * QR tree (RRF_ERR_SHAPE only beyond it).  Synchronises the plan's stream;
+ * RRF_ERR_INTERNAL if a grid-wide wait gave up (outputs undefined). */
 rrf_status rrf_panel_qr(rrf_plan_t plan, const void* Y, int64_t m, int64_t b,
                         int64_t ldy, void* V, int64_t ldv, void* T,
                         int64_t ldt, void* tau);
@@ -185,8 +202,9 @@ rrf_status rrf_panel_qr(rrf_plan_t plan, const void* Y, int64_t m, int64_t b,
 /* Block reflector application (Alg. 2, update step; LAPACK larfb with
  * side L, direct F, storev C):  X <- (I - V T V^T)^T X if trans != 0,
  * X <- (I - V T V^T) X if trans == 0.  V: m x b (ldv), T: b x b upper (ldt),
- * X: m x n (ldx), updated in place.  Requires b <= block_b_max,
- * m <= m_max, n <= n_max. */
+ * X: m x n (ldx), updated in place.  Requires b <= min(block_b_max, 64),
+ * m <= m_max, n <= n_max.  For binary64 X of at most 64 columns the call
+ * synchronises and returns RRF_ERR_INTERNAL if its grid-wide wait gave up. */
 rrf_status rrf_apply_block_reflector(rrf_plan_t plan, int trans,
                                      const void* V, int64_t ldv,
                                      const void* T, int64_t ldt, int64_t b,

@@ -40,6 +40,9 @@ constexpr int kPanelTsqr = 1;      // tall-skinny QR + Householder reconstructio
 constexpr int kPanelGram = 2;      // column recurrence from the Gram matrix, one exchange per sweep
 constexpr int kPanelAuto = 3;      // kPanelGram for blocks of <= 32 columns, else kPanelGrid
 constexpr int kTLd = 64;          // T stored like geqrt's T: 64 rows
+// Poll rounds before a grid-wide wait gives up (each a short sleep plus a
+// trip to the coherent memory path: tens of seconds in all).
+constexpr unsigned kSpinLimit = 1u << 24;
 
 struct Sizes {
   int64_t ldb, kcap, kcols;
@@ -95,6 +98,13 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
 
 }  // namespace
 
+// Work credited to a stage for the sub-block that starts at column col.
+struct SpecWork {
+  int stage;
+  int64_t col;
+  double flops, bytes;
+};
+
 struct rrf_plan {
   rrf_dtype dtype;
   size_t elem;
@@ -113,12 +123,14 @@ struct rrf_plan {
   DevState* st;
   DevState* st_host;
   int stop_mode, timing, panel_target;
+  unsigned spin_limit;       // poll rounds of a grid-wide wait (run state)
   unsigned panel_launches;   // epochs of the panel's tagged partials
   // last run
   int64_t last_m, last_n, last_k, last_b, nblocks;
   double E0, sigma2;
   std::vector<double> trace_trail, trace_sub;
-  std::vector<int64_t> block_start;
+  std::vector<int64_t> sub_start;   // first column of each sub-block of the last run
+  std::vector<SpecWork> spec;       // speculative credits of the last run
   double ms[RRF_NUM_STAGES], flops[RRF_NUM_STAGES], bytes[RRF_NUM_STAGES];
   int64_t launches[RRF_NUM_STAGES];
   std::vector<hipEvent_t> events;
@@ -271,8 +283,6 @@ hipError_t read_state(rrf_plan* p) {
   return hipStreamSynchronize(p->stream);
 }
 
-// Panel QR of the gathered panel pa.Y (m x b) into pa.V, pa.Tm, pa.tau with
-// the plan's panel algorithm (pa.Y is overwritten by the tall-skinny QR).
 // The panel algorithm for a block of b columns.  Narrow panels take the Gram
 // form (its column steps are cheap at 32 columns and it exchanges once per
 // sweep); 64-column panels take the column-by-column grid, which the
@@ -281,12 +291,33 @@ int panel_alg(const rrf_plan* p, int64_t b) {
   if (p->panel_mode != kPanelAuto) return p->panel_mode;
   return pad16(b) <= 32 ? kPanelGram : kPanelGrid;
 }
-bool panel_fits(rrf_plan* p, int64_t m, int b, PanelShape* sh) {
-  if (panel_alg(p, b) == kPanelGram) return gram_panel_shape(m, b, p->num_cus, sh);
-  return panel_shape(m, b, p->num_cus, p->panel_target, sh);
+
+// The route an m x b panel takes: the plan's algorithm when its
+// register-resident grid fits on the device, else the tall-skinny QR, whose
+// tree has no register-capacity bound (Alg. 2 puts no limit on m).  -1 if
+// no route fits (beyond the tree's depth).  sh->rows_pad is the row count
+// the gathered panel must cover.
+int panel_route(const rrf_plan* p, int64_t m, int b, PanelShape* sh) {
+  const int alg = panel_alg(p, b);
+  if (alg == kPanelGram && gram_panel_shape(m, b, p->num_cus, sh)) return kPanelGram;
+  if (alg == kPanelGrid && panel_shape(m, b, p->num_cus, p->panel_target, sh)) return kPanelGrid;
+  TsqrShape ts;
+  if (!tsqr_shape(m, b, &ts)) return -1;
+  sh->bp = ts.bp;
+  sh->rpt = 0;
+  sh->G = 0;
+  sh->rows_pad = ts.rows_pad;
+  return kPanelTsqr;
 }
-hipError_t run_panel(rrf_plan* p, PanelArgs& pa, const PanelShape& sh, hipStream_t s) {
-  const int alg = panel_alg(p, pa.b);
+bool panel_fits(const rrf_plan* p, int64_t m, int b, PanelShape* sh) {
+  return panel_route(p, m, b, sh) >= 0;
+}
+
+// Panel QR of the gathered panel pa.Y (m x b) into pa.V, pa.Tm, pa.tau by
+// route alg (from panel_route, with sh its shape; pa.Y is overwritten by the
+// tall-skinny QR).
+hipError_t run_panel(rrf_plan* p, PanelArgs& pa, int alg, const PanelShape& sh,
+                     hipStream_t s) {
   if (alg == kPanelGram) {
     GramPanelArgs ga{};
     ga.p = pa;
@@ -300,8 +331,15 @@ hipError_t run_panel(rrf_plan* p, PanelArgs& pa, const PanelShape& sh, hipStream
     if (!tsqr_shape(pa.m, pa.b, &ts)) return hipErrorInvalidValue;
     return launch_panel_tsqr(pa, ts, p->tsqr, s);
   }
+  if (alg != kPanelGrid) return hipErrorInvalidValue;
   pa.epoch_base = next_epoch(p);
   return launch_panel(pa, sh, s);
+}
+
+// A grid-wide wait that gave up stays recorded in the run state until
+// cleared; entry points clear it before their own launches.
+hipError_t clear_wait_error(rrf_plan* p) {
+  return hipMemsetAsync(&p->st->barrier_err, 0, sizeof(int), p->stream);
 }
 
 // X (mr x ncols) <- (I - V T V^T)^T X (trans) or (I - V T V^T) X, with V, T
@@ -371,11 +409,30 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   const int mode = p->stop_mode;
   p->trace_trail.clear();
   p->trace_sub.clear();
-  p->block_start.clear();
+  p->sub_start.clear();
+  p->spec.clear();
   p->nblocks = 0;
 
+  // Blocks of b columns (the last one ragged at k_cap) run as sub-blocks of
+  // at most 64 columns: Householder QR is column by column, so factoring a
+  // block's first 64 columns, updating, and sampling the rest from the
+  // updated B gives the block's reflectors (Q_1^T (B Omega_2) =
+  // (Q_1^T B) Omega_2).  The stop test runs at the end of each block only.
+  auto sub_width = [&](int64_t kk) -> int64_t {
+    if (kk >= kcap) return 0;
+    const int64_t be = std::min((kk / b) * b + b, kcap);
+    return std::min<int64_t>(kMaxBlock, be - kk);
+  };
+  // Work credited to a stage for the sub-block that starts at column col,
+  // taken back after the run if the run stopped before that sub-block (a
+  // sample, panel or W queued ahead of the stop test that the method never
+  // used).
+  auto spec = [&](int stage, int64_t col, double fl, double by) {
+    p->spec.push_back(SpecWork{stage, col, fl, by});
+  };
+
   // Initial sample Y_0 = A Omega_0 and ||A||_F^2 in one read of A.
-  const int64_t b0 = std::min(b, kcap);
+  const int64_t b0 = sub_width(0);
   const int q0 = b0 > 0 ? pad16(b0) : 0;
   if (b0 > 0)
     RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b0,
@@ -402,31 +459,33 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   if (p->st_host->nonfinite) return RRF_ERR_NONFINITE;
 
   // Look-ahead (the paper's two-queue overlap, Sec. 5, on one GPU): the
-  // update of block i samples Omega_{i+2} instead of Omega_{i+1}; the sample
-  // for block i + 1 is the one the previous update took, S_{i+1} = B^(i)
-  // Omega_{i+1}, brought up to date with the redundant panel update
-  // Y_{i+1} = Q_i^T S_{i+1} as soon as W_i exists (Q_i^T (B Omega) =
-  // (Q_i^T B) Omega).  The panel of block i + 1 is then factored by a few
-  // workgroups of the update's own launch while the rest update B.
+  // update of sub-block i samples Omega_{i+2} instead of Omega_{i+1}; the
+  // sample for sub-block i + 1 is the one the previous update took,
+  // S_{i+1} = B^(i) Omega_{i+1}, brought up to date with the redundant panel
+  // update Y_{i+1} = Q_i^T S_{i+1} as soon as W_i exists (Q_i^T (B Omega) =
+  // (Q_i^T B) Omega).  The panel of sub-block i + 1 is then factored by a
+  // few workgroups of the update's own launch while the rest update B.
   // It pays when the panel grid is small: a panel of more than a quarter of
   // the compute units takes too many slots from the update it runs beside.
-  bool la = p->lookahead != 0 && panel_alg(p, b) == kPanelGrid && kcap > b;
+  bool la = p->lookahead != 0 && panel_alg(p, b0) == kPanelGrid && kcap > b0;
   if (la) {
     PanelShape sh1;
-    la = panel_shape(m - b, (int)std::min(b, kcap - b), p->num_cus, p->panel_target, &sh1) &&
+    la = panel_shape(m - b0, (int)sub_width(b0), p->num_cus, p->panel_target, &sh1) &&
          sh1.G <= p->num_cus / 4;
   }
   int64_t k = 0;
   int64_t yoff = 0;          // row offset of the next sample in the slabs
-  int blk = 0;
-  bool panel_ready = false;  // the panel of this block was factored by the last update
+  int blk = 0;               // blocks finished (stop tests run)
+  int sub = 0;               // sub-blocks started
+  bool panel_ready = false;  // the panel of this sub-block was factored by the last update
   bool stop = p->st_host->stop != 0;
-  bool w_ready = false;      // W of this block was formed at the end of the last one
+  bool w_ready = false;      // W of this sub-block was formed at the end of the last one
   double E_prev2 = 0.0;      // the stopping quantity one state read earlier
 
-  // Z = V^T B[kk:m, :] and W = T^T Z of the block at kk (width bb), from the
-  // rows kk..m of sx.
-  auto issue_w = [&](int64_t kk, int64_t bb, const T* sx, int64_t ldsx) -> rrf_status {
+  // Z = V^T B[kk:m, :] and W = T^T Z of the sub-block at kk (width bb),
+  // from the rows kk..m of sx; speculative when queued ahead of a stop test.
+  auto issue_w = [&](int64_t kk, int64_t bb, const T* sx, int64_t ldsx,
+                     bool speculative) -> rrf_status {
     const int64_t mpp = m - kk;
     const int bpp = pad16(bb);
     const int sr0 = red_splits(mpp, n, p->num_cus);
@@ -436,30 +495,39 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     ra.Z = (T*)p->Zpart; ra.split_stride = n * bpp;
     ra.rows_per_split = round_up(ceil_div(mpp, sr0), kRedChunk);
     const int sr = (int)ceil_div(mpp, ra.rows_per_split);
-    RRF_LAUNCH(p, RRF_STAGE_REDUCE, 2.0 * mpp * n * bb, e * mpp * n,
-               launch_reduce<T>(ra, sr, s));
+    const double rfl = 2.0 * mpp * n * bb, rby = e * mpp * n;
+    RRF_LAUNCH(p, RRF_STAGE_REDUCE, rfl, rby, launch_reduce<T>(ra, sr, s));
     FormWArgs<T> fa{};
     fa.Z = (T*)p->Zpart; fa.nsplit = sr; fa.split_stride = ra.split_stride;
     fa.Tm = Tm + kk * kTLd; fa.ldt = kTLd; fa.W = (T*)p->W; fa.n = n; fa.bp = bpp;
     fa.trans = 1;
     fa.b = (int)bb;
-    RRF_LAUNCH(p, RRF_STAGE_FORMW, 1.0 * n * bb * bb, e * n * bb * (sr + 1),
-               launch_formw<T>(fa, s));
+    const double wfl = 1.0 * n * bb * bb, wby = e * n * bb * (sr + 1);
+    RRF_LAUNCH(p, RRF_STAGE_FORMW, wfl, wby, launch_formw<T>(fa, s));
+    if (speculative) {
+      spec(RRF_STAGE_REDUCE, kk, rfl, rby);
+      spec(RRF_STAGE_FORMW, kk, wfl, wby);
+    }
     return RRF_OK;
   };
+  auto panel_flops = [](double mr, double bb) {
+    return 2.0 * mr * bb * bb - 2.0 / 3.0 * bb * bb * bb + 1.0 * mr * bb * bb;
+  };
   while (!stop) {
-    const int64_t bi = std::min(b, kcap - k);
+    const int64_t bi = sub_width(k);
     const int bp = pad16(bi);
     const int64_t mp = m - k;
-    p->block_start.push_back(k);
+    p->sub_start.push_back(k);
     const int64_t k_next = k + bi;
-    const int64_t b_next = k_next < kcap ? std::min(b, kcap - k_next) : 0;
-    bool s1_done = false;      // block 0: S_1 = A Omega_1 taken with the panel
+    const bool at_end = k_next == kcap || k_next % b == 0;   // a stop test follows
+    const int64_t b_next = sub_width(k_next);
+    bool s1_done = false;      // sub-block 0: S_1 = A Omega_1 taken with the panel
     if (panel_ready) {
       panel_ready = false;
     } else {
       PanelShape sh;
-      if (!panel_fits(p, mp, (int)bi, &sh)) return RRF_ERR_SHAPE;
+      const int route = panel_route(p, mp, (int)bi, &sh);
+      if (route < 0) return RRF_ERR_SHAPE;
       RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mp * bi * ysplits + 8.0 * mp * bi,
                  launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
                                         (int)bi, bp, sh.rows_pad, p->Ysum,
@@ -470,19 +538,19 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       pa.V = V + k + k * ldb; pa.ldv = ldb;
       pa.Tm = Tm + k * kTLd; pa.ldt = kTLd; pa.tau = tau + k;
       pa.red = p->red; pa.rowj = p->rowj; pa.st = p->st; pa.G = sh.G;
-      const double pflops =
-          2.0 * mp * bi * bi - 2.0 / 3.0 * bi * bi * bi + 1.0 * mp * bi * bi;
-      const int occ0 = la && blk == 0 && b_next > 0 && pad16(b_next) == 64 &&
-                               panel_alg(p, (int)bi) == kPanelGrid &&
-                               sample_panel_supported(64, sh)
+      const double pflops = panel_flops((double)mp, (double)bi);
+      const int occ0 = la && sub == 0 && b_next > 0 && pad16(b_next) == 64 &&
+                               route == kPanelGrid && sample_panel_supported(64, sh)
                            ? sample_panel_occupancy<T>(sh) : 0;
       if (occ0 > 0 && (int64_t)occ0 * p->num_cus > sh.G) {
-        // Look-ahead, block 0: the panel of block 0 and the first look-ahead
-        // sample S_1 = A Omega_1 (independent of it) in one launch.  The
-        // gather above has already read the partials of Y_0 that S_1 replaces.
+        // Look-ahead, sub-block 0: the panel of sub-block 0 and the first
+        // look-ahead sample S_1 = A Omega_1 (independent of it) in one
+        // launch.  The gather above has already read the partials of Y_0
+        // that S_1 replaces.
         RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
                    launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_next, b_next,
                                     Om, kOmLd, 1, s));
+        spec(RRF_STAGE_SKETCH, k_next, 0.0, e * n * b_next);
         UpdateArgs<T> u1 = u;
         u1.qp = 64;
         u1.normpart = nullptr;
@@ -490,32 +558,36 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
         u1.cols_per_split = round_up(ceil_div(n, su1), kUpdChunk);
         const int ys1 = (int)ceil_div(n, u1.cols_per_split);
         pa.epoch_base = next_epoch(p);
-        RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 2.0 * m * n * b_next + pflops,
-                   e * (m * n + m * b_next) + 16.0 * mp * bi,
+        const double sfl = 2.0 * m * n * b_next, sby = e * (m * n + m * b_next);
+        RRF_LAUNCH(p, RRF_STAGE_SAMPLE, sfl + pflops, sby + 16.0 * mp * bi,
                    launch_sample_panel<T>(u1, ys1, pa, sh, s));
+        spec(RRF_STAGE_SAMPLE, k_next, sfl, sby);
         ysplits = ys1;
         yoff = 0;
         s1_done = true;
       } else {
-        RRF_LAUNCH(p, RRF_STAGE_PANEL, pflops, 16.0 * mp * bi, run_panel(p, pa, sh, s));
+        RRF_LAUNCH(p, RRF_STAGE_PANEL, pflops, 16.0 * mp * bi,
+                   run_panel(p, pa, route, sh, s));
       }
     }
 
-    const T* src = blk == 0 ? A : Bws;
-    const int64_t lsrc = blk == 0 ? lda : ldb;
+    const T* src = sub == 0 ? A : Bws;
+    const int64_t lsrc = sub == 0 ? lda : ldb;
 
-    // Look-ahead, block 0: S_1 = A Omega_1 if it was not taken with the panel
-    // above (later blocks get their look-ahead sample from the previous
-    // update).
-    if (la && blk == 0 && b_next > 0 && !s1_done) {
+    // Look-ahead, sub-block 0: S_1 = A Omega_1 if it was not taken with the
+    // panel above (later sub-blocks get their look-ahead sample from the
+    // previous update).
+    if (la && sub == 0 && b_next > 0 && !s1_done) {
       RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
                  launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_next, b_next,
                                   Om, kOmLd, 1, s));
+      spec(RRF_STAGE_SKETCH, k_next, 0.0, e * n * b_next);
       UpdateArgs<T> u1 = u;
       u1.qp = pad16(b_next);
       u1.normpart = nullptr;
-      RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 2.0 * m * n * b_next, e * (m * n + m * b_next),
-                 launch_update<T>(u1, ysplits, s));
+      const double sfl = 2.0 * m * n * b_next, sby = e * (m * n + m * b_next);
+      RRF_LAUNCH(p, RRF_STAGE_SAMPLE, sfl, sby, launch_update<T>(u1, ysplits, s));
+      spec(RRF_STAGE_SAMPLE, k_next, sfl, sby);
       yoff = 0;
     }
 
@@ -524,11 +596,11 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     if (w_ready) {
       w_ready = false;
     } else {
-      rrf_status rs = issue_w(k, bi, src, lsrc);
+      rrf_status rs = issue_w(k, bi, src, lsrc, false);
       if (rs != RRF_OK) return rs;
     }
 
-    PanelArgs pan{};          // look-ahead panel of block i + 1
+    PanelArgs pan{};          // look-ahead panel of sub-block i + 1
     PanelShape pan_shape{};
     double pan_flops = 0.0, pan_bytes = 0.0;
     if (la && b_next > 0) {
@@ -539,26 +611,28 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       PanelShape shn;
       if (!panel_shape(mpn, (int)b_next, p->num_cus, p->panel_target, &shn))
         return RRF_ERR_SHAPE;
-      RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mp * b_next * ysplits + 8.0 * mp * b_next,
+      const double gby = e * mp * b_next * ysplits + 8.0 * mp * b_next;
+      RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, gby,
                  launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
                                         (int)b_next, bpn, bi + shn.rows_pad,
                                         p->Ysum, p->sz.ldysum, s));
+      spec(RRF_STAGE_PANEL, k_next, 0.0, gby);
       ThinApplyArgs ta{};
       ta.V = V + k + k * ldb; ta.ldv = ldb;
       ta.Tm = Tm + k * kTLd; ta.ldt = kTLd; ta.b = (int)bi; ta.trans = 1;
       ta.Y = p->Ysum; ta.ldy = p->sz.ldysum; ta.mr = mp; ta.ncols = (int)b_next;
       ta.part = p->tx; ta.sums = p->tx + kThinPartWords;
       ta.epoch_base = next_epoch(p); ta.st = p->st;
-      RRF_LAUNCH(p, RRF_STAGE_PANEL, 4.0 * mp * bi * b_next, 16.0 * mp * b_next + 8.0 * mp * bi,
-                 launch_thin_apply(ta, p->num_cus, s));
+      const double tfl = 4.0 * mp * bi * b_next, tby = 16.0 * mp * b_next + 8.0 * mp * bi;
+      RRF_LAUNCH(p, RRF_STAGE_PANEL, tfl, tby, launch_thin_apply(ta, p->num_cus, s));
+      spec(RRF_STAGE_PANEL, k_next, tfl, tby);
       pan.Y = p->Ysum + bi; pan.ldy = p->sz.ldysum;
       pan.m = mpn; pan.b = (int)b_next;
       pan.V = V + k_next + k_next * ldb; pan.ldv = ldb;
       pan.Tm = Tm + k_next * kTLd; pan.ldt = kTLd; pan.tau = tau + k_next;
       pan.red = p->red; pan.rowj = p->rowj; pan.st = p->st; pan.G = shn.G;
       pan_shape = shn;
-      pan_flops = 2.0 * mpn * b_next * b_next - 2.0 / 3.0 * b_next * b_next * b_next +
-                  1.0 * mpn * b_next * b_next;
+      pan_flops = panel_flops((double)mpn, (double)b_next);
       pan_bytes = 16.0 * mpn * b_next;
       panel_ready = true;
     }
@@ -566,13 +640,14 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     // Sketch block sampled by this update (speculative: the stop test comes
     // after the update): Omega_{i+1}, or Omega_{i+2} with look-ahead.
     const int64_t k_s = la ? k_next + b_next : k_next;
-    const int64_t b_s = (la ? (b_next > 0 && k_s < kcap) : b_next > 0)
-                            ? std::min(b, kcap - k_s) : 0;
+    const int64_t b_s = (la ? b_next > 0 : true) ? sub_width(k_s) : 0;
     const int q_s = b_s > 0 ? pad16(b_s) : 0;
-    if (b_s > 0)
+    if (b_s > 0) {
       RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_s,
                  launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_s, b_s, Om,
                                   kOmLd, 1, s));
+      spec(RRF_STAGE_SKETCH, k_s, 0.0, e * n * b_s);
+    }
 
     // B[k:m, :] -= V_i W, fused with the sample and the norms.
     UpdateArgs<T> ua{};
@@ -590,27 +665,41 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     }
     ua.cols_per_split = round_up(ceil_div(n, su0), kUpdChunk);
     const int su = (int)ceil_div(n, ua.cols_per_split);
-    const double upd_flops = 2.0 * mp * n * bi + 2.0 * (mp - bi) * n * b_s;
+    const double smp_flops = 2.0 * (mp - bi) * n * b_s;
+    const double upd_flops = 2.0 * mp * n * bi + smp_flops;
     if (panel_ready) {
       pan.epoch_base = next_epoch(p);
       if (fused) {
         RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops + pan_flops,
                    2.0 * e * mp * n + pan_bytes,
                    launch_update_panel<T>(ua, su, pan, pan_shape, s));
+        spec(RRF_STAGE_UPDATE, k_next, pan_flops, pan_bytes);
       } else {
         RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops, 2.0 * e * mp * n,
                    launch_update<T>(ua, su, s));
         RRF_LAUNCH(p, RRF_STAGE_PANEL, pan_flops, pan_bytes,
-                   run_panel(p, pan, pan_shape, s));
+                   run_panel(p, pan, kPanelGrid, pan_shape, s));
+        spec(RRF_STAGE_PANEL, k_next, pan_flops, pan_bytes);
       }
     } else {
       RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops, 2.0 * e * mp * n,
                  launch_update<T>(ua, su, s));
     }
+    if (b_s > 0) spec(RRF_STAGE_UPDATE, k_s, smp_flops, 0.0);
     nparts = (int)(ceil_div(mp, kUpdRows) * su);
     RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
                launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
-                               p->trace_sub_d, blk, k_next, kcap, mode, tol, 0, s));
+                               p->trace_sub_d, at_end ? blk : -1, k_next, kcap,
+                               mode, tol, 0, s));
+    if (!at_end) {
+      // Inside a block: the next sub-block runs whatever the norms say (an
+      // error recorded meanwhile is read at the end of the block).
+      k = k_next;
+      ++sub;
+      yoff = bi;
+      ysplits = su;
+      continue;
+    }
     // Work for the next block that does not depend on the stop test is
     // queued behind the copy of the run state, and the host waits for the
     // copy alone, so the device keeps working while the host reads the test:
@@ -628,7 +717,11 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     const bool more_likely = b_next > 0 && E_pred > p->st_host->sigma2;
     bool next_panel = false, next_w = false;
     PanelShape shn{};
-    if (!la && more_likely && panel_fits(p, m - k_next, (int)b_next, &shn)) next_panel = true;
+    int route_n = -1;
+    if (!la && more_likely) {
+      route_n = panel_route(p, m - k_next, (int)b_next, &shn);
+      next_panel = route_n >= 0;
+    }
     if (la && more_likely && panel_ready) next_w = true;
     if ((next_panel || next_w) && !p->state_ev) {
       he = hipEventCreateWithFlags(&p->state_ev, hipEventDisableTiming);
@@ -641,12 +734,13 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       if (he != hipSuccess) return hip_fail(he);
     }
     if (next_w) {
-      rrf_status rs = issue_w(k_next, b_next, Bws, ldb);
+      rrf_status rs = issue_w(k_next, b_next, Bws, ldb, true);
       if (rs != RRF_OK) return rs;
     }
     if (next_panel) {
       const int64_t mpn = m - k_next;
-      RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, e * mpn * b_next * su + 8.0 * mpn * b_next,
+      const double gby = e * mpn * b_next * su + 8.0 * mpn * b_next;
+      RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, gby,
                  launch_gather_panel<T>(Yp + bi, ldb, ldb * 64, su, mpn, (int)b_next,
                                         pad16(b_next), shn.rows_pad, p->Ysum,
                                         p->sz.ldysum, s));
@@ -656,15 +750,15 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       pn.V = V + k_next + k_next * ldb; pn.ldv = ldb;
       pn.Tm = Tm + k_next * kTLd; pn.ldt = kTLd; pn.tau = tau + k_next;
       pn.red = p->red; pn.rowj = p->rowj; pn.st = p->st; pn.G = shn.G;
-      RRF_LAUNCH(p, RRF_STAGE_PANEL,
-                 2.0 * mpn * b_next * b_next - 2.0 / 3.0 * b_next * b_next * b_next +
-                     1.0 * mpn * b_next * b_next,
-                 16.0 * mpn * b_next, run_panel(p, pn, shn, s));
+      const double pfl = panel_flops((double)mpn, (double)b_next), pby = 16.0 * mpn * b_next;
+      RRF_LAUNCH(p, RRF_STAGE_PANEL, pfl, pby, run_panel(p, pn, route_n, shn, s));
+      spec(RRF_STAGE_PANEL, k_next, pfl, pby + gby);
     }
     he = (next_panel || next_w) ? hipEventSynchronize(p->state_ev) : hipStreamSynchronize(s);
     if (he != hipSuccess) return hip_fail(he);
     k = k_next;
     ++blk;
+    ++sub;
     yoff = bi;
     ysplits = su;
     if (next_panel) panel_ready = true;
@@ -675,17 +769,18 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   }
   p->nblocks = blk;
 
-  // Explicit Q = H_0 ... H_{k-1} [I_k; 0], backward over the blocks, in
+  // Explicit Q = H_0 ... H_{k-1} [I_k; 0], backward over the sub-blocks, in
   // binary64 (float plans round the result once).
+  const int nsub = (int)p->sub_start.size();
   if (k > 0) {
     double* Qd = std::is_same<T, double>::value ? (double*)Q : (double*)p->Q64;
     RRF_LAUNCH(p, RRF_STAGE_ORGQR, 0.0, 8.0 * m * k,
                launch_fill_identity<double>(Qd, ldb, m, k, s));
-    for (int i = blk - 1; i >= 0; --i) {
-      const int64_t ki = p->block_start[i];
-      const int64_t bi = (i + 1 < blk ? p->block_start[i + 1] : k) - ki;
+    for (int i = nsub - 1; i >= 0; --i) {
+      const int64_t ki = p->sub_start[i];
+      const int64_t bi = (i + 1 < nsub ? p->sub_start[i + 1] : k) - ki;
       if (k - ki <= 64) {
-        // The last block's columns alone: the one-launch thin kernel.
+        // The last sub-block's columns alone: the one-launch thin kernel.
         ThinApplyArgs ta{};
         ta.V = V + ki + ki * ldb; ta.ldv = ldb;
         ta.Tm = Tm + ki * kTLd; ta.ldt = kTLd; ta.b = (int)bi; ta.trans = 0;
@@ -710,10 +805,18 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   he = hipStreamSynchronize(s);
   if (he != hipSuccess) return hip_fail(he);
   if (k > 0) {
-    // The thin kernel's grid exchange (last block) reports a wait that ran out.
+    // Errors recorded after the last state read: the thin kernel's grid
+    // exchange (last sub-block of Q).
     he = read_state(p);
     if (he != hipSuccess) return hip_fail(he);
     if (p->st_host->barrier_err) return RRF_ERR_INTERNAL;
+    if (p->st_host->nonfinite) return RRF_ERR_NONFINITE;
+  }
+  // Take back the credit of work queued for sub-blocks past k.
+  for (const SpecWork& w : p->spec) {
+    if (w.col < k) continue;
+    p->flops[w.stage] -= w.flops;
+    p->bytes[w.stage] -= w.bytes;
   }
 
   // Trace back to the host.
@@ -758,22 +861,28 @@ rrf_status panel_stage(rrf_plan* p, const T* Y, int64_t m, int64_t b,
                        int64_t ldy, T* Vout, int64_t ldv, T* Tout, int64_t ldt,
                        T* tauout) {
   PanelShape sh;
-  if (!panel_fits(p, m, (int)b, &sh)) return RRF_ERR_SHAPE;
+  const int route = panel_route(p, m, (int)b, &sh);
+  if (route < 0) return RRF_ERR_SHAPE;
   hipStream_t s = p->stream;
-  hipError_t e0 = launch_gather_panel<T>(Y, ldy, 0, 1, m, (int)b, sh.bp,
-                                         sh.rows_pad, p->Ysum, p->sz.ldysum, s);
-  if (e0 != hipSuccess) return hip_fail(e0);
+  hipError_t e = clear_wait_error(p);
+  if (e == hipSuccess)
+    e = launch_gather_panel<T>(Y, ldy, 0, 1, m, (int)b, sh.bp, sh.rows_pad, p->Ysum,
+                               p->sz.ldysum, s);
+  if (e != hipSuccess) return hip_fail(e);
   PanelArgs pa{};
   pa.Y = p->Ysum; pa.ldy = p->sz.ldysum;
   pa.m = m; pa.b = (int)b;
   pa.V = p->V; pa.ldv = p->sz.ldb;
   pa.Tm = p->Tm; pa.ldt = kTLd; pa.tau = p->tau;
   pa.red = p->red; pa.rowj = p->rowj; pa.st = p->st; pa.G = sh.G;
-  hipError_t e = run_panel(p, pa, sh, s);
+  e = run_panel(p, pa, route, sh, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->V, p->sz.ldb, Vout, ldv, m, b, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->Tm, kTLd, Tout, ldt, b, b, s);
   if (e == hipSuccess) e = to_plan_type<T>(p->tau, 1, tauout, 1, b, 1, s);
-  return e == hipSuccess ? RRF_OK : hip_fail(e);
+  // A grid-wide wait that gave up leaves V, T and tau undefined.
+  if (e == hipSuccess) e = read_state(p);
+  if (e != hipSuccess) return hip_fail(e);
+  return p->st_host->barrier_err ? RRF_ERR_INTERNAL : RRF_OK;
 }
 
 template <typename T>
@@ -800,7 +909,8 @@ rrf_status larfb_stage(rrf_plan* p, int trans, const T* V, int64_t ldv,
     ta.Y = (double*)X; ta.ldy = ldx; ta.mr = m; ta.ncols = (int)n;
     ta.part = p->tx; ta.sums = p->tx + kThinPartWords;
     ta.epoch_base = next_epoch(p); ta.st = p->st;
-    e = launch_thin_apply(ta, p->num_cus, s);
+    e = clear_wait_error(p);
+    if (e == hipSuccess) e = launch_thin_apply(ta, p->num_cus, s);
     if (e == hipSuccess) e = read_state(p);
     if (e != hipSuccess) return hip_fail(e);
     return p->st_host->barrier_err ? RRF_ERR_INTERNAL : RRF_OK;
@@ -831,7 +941,7 @@ rrf_status rrf_workspace_size(rrf_dtype dtype, int64_t m_max, int64_t n_max,
                               int64_t block_b_max, int64_t k_max,
                               size_t* bytes) {
   if (!bytes || !valid_dtype(dtype) || m_max < 1 || n_max < 1 ||
-      block_b_max < 1 || block_b_max > kMaxBlock || k_max < 0)
+      block_b_max < 1 || block_b_max > kMaxBlockB || k_max < 0)
     return RRF_ERR_INVALID_ARG;
   *bytes = compute_sizes(dtype, m_max, n_max, block_b_max, k_max).total();
   return RRF_OK;
@@ -841,7 +951,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
                            int64_t n_max, int64_t block_b_max, int64_t k_max,
                            void* hip_stream) {
   if (!plan || !valid_dtype(dtype) || m_max < 1 || n_max < 1 ||
-      block_b_max < 1 || block_b_max > kMaxBlock || k_max < 0)
+      block_b_max < 1 || block_b_max > kMaxBlockB || k_max < 0)
     return RRF_ERR_INVALID_ARG;
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return RRF_ERR_HIP;
@@ -883,9 +993,19 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
     free_plan(p);
     return RRF_ERR_HIP;
   }
-  // The first panel has m_max rows; it must fit the register-resident panel.
+  // RRF_TEST_SPIN_LIMIT sets the poll rounds of every grid-wide wait of the
+  // plan (tests: 0 makes each wait give up at its first poll, so the
+  // give-up path runs while every kernel still drains).
+  p->spin_limit = kSpinLimit;
+  if (const char* sl = std::getenv("RRF_TEST_SPIN_LIMIT")) {
+    const long v = std::atol(sl);
+    if (v >= 0 && v <= (long)kSpinLimit) p->spin_limit = (unsigned)v;
+  }
+  // The first panel has m_max rows; some route must fit it (sub-blocks have
+  // at most 64 columns).
   PanelShape sh;
-  if (!panel_fits(p, std::max(m_max, block_b_max), (int)block_b_max, &sh)) {
+  const int64_t b_sub = std::min<int64_t>(block_b_max, kMaxBlock);
+  if (!panel_fits(p, std::max(m_max, b_sub), (int)b_sub, &sh)) {
     free_plan(p);
     return RRF_ERR_SHAPE;
   }
@@ -931,7 +1051,12 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   if (e == hipSuccess) e = hipMemsetAsync(p->rowj, 0, p->sz.rowj, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->gx, 0, p->sz.gx, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->tx, 0, p->sz.tx, p->stream);
-  if (e == hipSuccess) e = hipMemsetAsync(p->st, 0, p->sz.st, p->stream);
+  if (e == hipSuccess) {
+    std::memset(p->st_host, 0, sizeof(DevState));
+    p->st_host->spin_limit = p->spin_limit;
+    e = hipMemcpyAsync(p->st, p->st_host, sizeof(DevState), hipMemcpyHostToDevice,
+                       p->stream);
+  }
   if (e == hipSuccess) e = hipMemsetAsync(p->Om, 0, p->sz.Om, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->V, 0, p->sz.V, p->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(p->stream);
@@ -1042,9 +1167,9 @@ rrf_status rrf_get_reflectors(rrf_plan_t plan, const void** V, int64_t* ldv,
   // Zero V above each block (the kernels never touch those rows).
   if (plan->last_k > 0) {
     const int64_t ldb = plan->sz.ldb;
-    for (size_t i = 0; i < plan->block_start.size(); ++i) {
-      const int64_t ki = plan->block_start[i];
-      const int64_t bi = (i + 1 < plan->block_start.size() ? plan->block_start[i + 1]
+    for (size_t i = 0; i < plan->sub_start.size(); ++i) {
+      const int64_t ki = plan->sub_start[i];
+      const int64_t bi = (i + 1 < plan->sub_start.size() ? plan->sub_start[i + 1]
                                                             : plan->last_k) - ki;
       if (ki == 0) continue;
       for (int64_t c = 0; c < bi; ++c) {
@@ -1085,7 +1210,8 @@ rrf_status rrf_panel_qr(rrf_plan_t plan, const void* Y, int64_t m, int64_t b,
                         int64_t ldy, void* V, int64_t ldv, void* T,
                         int64_t ldt, void* tau) {
   if (!plan || !Y || !V || !T || !tau) return RRF_ERR_INVALID_ARG;
-  if (b < 1 || b > plan->b_max || m < b || ldy < m || ldv < m || ldt < b)
+  if (b < 1 || b > std::min<int64_t>(plan->b_max, kMaxBlock) || m < b || ldy < m || ldv < m ||
+      ldt < b)
     return RRF_ERR_INVALID_ARG;
   if (m > plan->m_max) return RRF_ERR_SHAPE;
   if (plan->dtype == RRF_F64)
@@ -1101,7 +1227,8 @@ rrf_status rrf_apply_block_reflector(rrf_plan_t plan, int trans,
                                      void* X, int64_t m, int64_t n,
                                      int64_t ldx) {
   if (!plan || !V || !T || !X) return RRF_ERR_INVALID_ARG;
-  if (b < 1 || b > plan->b_max || m < 0 || n < 0 || ldv < std::max<int64_t>(1, m) ||
+  if (b < 1 || b > std::min<int64_t>(plan->b_max, kMaxBlock) || m < 0 || n < 0 ||
+      ldv < std::max<int64_t>(1, m) ||
       ldt < b || ldx < std::max<int64_t>(1, m))
     return RRF_ERR_INVALID_ARG;
   if (m > plan->m_max || n > plan->n_max) return RRF_ERR_SHAPE;

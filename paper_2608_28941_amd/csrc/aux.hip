@@ -9,10 +9,12 @@ namespace {
 // Sums the per-workgroup norm partials in a fixed order (deterministic) and
 // applies the stop test.  init: E0 = ||A||_F^2, sigma^2 = tol^2 E0.
 // Otherwise: E_trail = ||B[k:m, :]||^2 directly, E_sub -= ||B_i||^2 (the
-// paper's running difference, clamped at 0); stop iff E <= sigma^2 or the
+// paper's running difference, clamped at 0).  At the end of a block (block
+// >= 0: the trace index) the stop test runs: stop iff E <= sigma^2 or the
 // rank cap is reached (Sec. 4: the loop ends after at most min(m, n) / b
-// blocks).  A NaN norm fails "E > sigma^2" and would stop silently, so
-// non-finite norms are flagged.
+// blocks); inside a block (block < 0, the first 64 columns of a wider
+// block) only errors stop.  A NaN norm fails "E > sigma^2" and would stop
+// silently, so non-finite norms are flagged.
 __global__ __launch_bounds__(256) void finalize_kernel(
     const double* np, int nparts, DevState* st, double* tt, double* ts,
     int block, int64_t k_after, int64_t k_cap, int mode, double tol, int init) {
@@ -48,12 +50,16 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     if (es < 0.0) es = 0.0;
     st->E_sub = es;
     st->E_trail = trail;
-    tt[block] = trail;
-    ts[block] = es;
     if (!isfinite(trail)) st->nonfinite = 1;
-    const double E = mode ? es : trail;
-    st->stop = st->nonfinite || st->barrier_err || !(E > st->sigma2) ||
-               k_after >= k_cap;
+    if (block >= 0) {
+      tt[block] = trail;
+      ts[block] = es;
+      const double E = mode ? es : trail;
+      st->stop = st->nonfinite || st->barrier_err || !(E > st->sigma2) ||
+                 k_after >= k_cap;
+    } else {
+      st->stop = st->nonfinite || st->barrier_err;
+    }
   }
 }
 

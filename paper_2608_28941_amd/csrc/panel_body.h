@@ -57,6 +57,7 @@ __device__ __forceinline__ void panel_body(const PanelArgs& a, const int w) {
   // The last workgroup collects V^T V and builds T at the end; workgroup 0
   // (which publishes row j every step) has no extra work.
   const bool tw = (w == a.G - 1);
+  const bool forced = waits_forced(a.st);
 
   // The gathered panel has G * RW rows and BP columns, zero outside (m, b),
   // so the RPT loads are unconditional and all in flight together.
@@ -150,7 +151,7 @@ __device__ __forceinline__ void panel_body(const PanelArgs& a, const int w) {
 #pragma unroll
           for (int u = 0; u < 16; ++u)
             ok = ok && tagged(hi[u], epoch) && tagged(lo[u], epoch);
-        } while (!ok && keep_waiting(&spins, a.st));
+        } while ((!ok || forced) && keep_waiting(&spins, a.st));
 #pragma unroll
         for (int u = 0; u < 16; ++u)
           if (w0 + u * GR < a.G) s += untag(hi[u], lo[u]);

@@ -103,6 +103,7 @@ __global__ __launch_bounds__(NT) void panel_gram_kernel(GramPanelArgs ga) {
   const int w = (int)blockIdx.x;
   const int64_t base = (int64_t)w * RW;
   const int b = a.b, G = a.G;
+  const bool forced = waits_forced(a.st);
 
   double col[RPT];
   {
@@ -213,7 +214,7 @@ __global__ __launch_bounds__(NT) void panel_gram_kernel(GramPanelArgs ga) {
               ok = true;
 #pragma unroll
               for (int u = 0; u < 8; ++u) ok = ok && tagged(hi[u], epoch) && tagged(lo[u], epoch);
-            } while (!ok && keep_waiting(&spins, a.st));
+            } while ((!ok || forced) && keep_waiting(&spins, a.st));
 #pragma unroll
             for (int u = 0; u < 8; ++u)
               if (w0 + u * nsub < G) s += untag(hi[u], lo[u]);
@@ -251,7 +252,7 @@ __global__ __launch_bounds__(NT) void panel_gram_kernel(GramPanelArgs ga) {
           ok = true;
 #pragma unroll
           for (int i = 0; i < NQ; ++i) ok = ok && tagged(hi[i], epoch) && tagged(lo[i], epoch);
-        } while (!ok && keep_waiting(&spins, a.st));
+        } while ((!ok || forced) && keep_waiting(&spins, a.st));
 #pragma unroll
         for (int i = 0; i < BR; ++i)
 #pragma unroll

@@ -10,7 +10,8 @@
 namespace rrf {
 
 // Tiling constants (see each kernel for its use).
-constexpr int kMaxBlock = 64;      // largest block size b (MFMA tiles of 16)
+constexpr int kMaxBlock = 64;      // widest sub-block / panel (MFMA tiles of 16)
+constexpr int kMaxBlockB = 128;    // largest block size b of a run (sub-blocks of <= 64)
 constexpr int kUpdRowTiles = 2;    // 16-row tiles per update wavefront
 constexpr int kUpdRows = 128;      // rows per update workgroup (4 waves x 2 x 16)
 constexpr int kUpdChunk = 16;      // columns per staged chunk in the update
@@ -32,8 +33,9 @@ struct DevState {
   double E_sub;     // running difference (paper's rule), clamped at 0
   int stop;         // 1: stop after this block
   int nonfinite;    // 1: a norm was NaN / Inf
-  int barrier_err;  // 1: a panel grid barrier gave up waiting
-  int pad;
+  int barrier_err;  // 1: a grid-wide wait gave up (sticky until cleared)
+  unsigned spin_limit;  // poll rounds before a grid-wide wait gives up; 0:
+                        // every wait gives up at its first poll (tests)
 };
 
 // Launch descriptors -------------------------------------------------------

@@ -38,6 +38,7 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
   const int64_t r_begin = (int64_t)w * a.rows_per_wg;
   const int64_t r_end = min(a.mr, r_begin + a.rows_per_wg);
   const unsigned epoch = a.epoch_base + 1u;
+  const bool forced = waits_forced(a.st);
 
   // T (leading b x b block, upper triangular) to LDS: all loads issued
   // before the first use (columns past b read column 0), entries outside the
@@ -133,7 +134,7 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
             ok = true;
 #pragma unroll
             for (int u = 0; u < 8; ++u) ok = ok && tagged(hi[u], epoch) && tagged(lo[u], epoch);
-          } while (!ok && keep_waiting(&spins, a.st));
+          } while ((!ok || forced) && keep_waiting(&spins, a.st));
 #pragma unroll
           for (int u = 0; u < 8; ++u)
             if (w0 + u * nsub < G) s += untag(hi[u], lo[u]);
@@ -166,7 +167,7 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
       ok = true;
 #pragma unroll
       for (int i = 0; i < NPT; ++i) ok = ok && tagged(hi[i], epoch) && tagged(lo[i], epoch);
-    } while (!ok && keep_waiting(&spins, a.st));
+    } while ((!ok || forced) && keep_waiting(&spins, a.st));
 #pragma unroll
     for (int i = 0; i < NPT; ++i) {
       const int e = t + 256 * i;

@@ -8,8 +8,6 @@
 namespace rrf {
 namespace {
 
-constexpr unsigned kSpinLimit = 1u << 24;
-
 // Cross-workgroup traffic uses agent-scope atomic accesses only (coherent
 // across the XCDs without L2 write-back or invalidation, which an
 // agent-scope fence would cost on every step).
@@ -25,9 +23,11 @@ constexpr unsigned kSpinLimit = 1u << 24;
 // plan creation and epoch 0 is never used), so words left by earlier steps
 // or launches never match.  A slot is rewritten two steps later only by a
 // workgroup that has seen every workgroup's next-step partials, so no reader
-// is still reading it.  The wait is bounded: after kSpinLimit polls it
-// records an error and every later wait returns at once, so the kernel
-// always drains (the results are then discarded by the host).
+// is still reading it.  The wait is bounded: after the run state's spin limit
+// (kSpinLimit polls, each a sleep of about 128 cycles plus a trip to the
+// coherent memory path: tens of seconds) it records an error and every later
+// wait returns at once, so the kernel always drains (the host then reports
+// RRF_ERR_INTERNAL and discards the results).
 typedef unsigned long long u64;
 
 __device__ __forceinline__ void put_tagged(u64* p, double v, unsigned epoch) {
@@ -48,17 +48,25 @@ __device__ __forceinline__ bool tagged(u64 w, unsigned epoch) {
 }
 
 // One poll round failed: back off, count, and give up (recording the error)
-// after kSpinLimit rounds or once another thread has given up.
+// after the run state's spin limit or once another thread has given up.  A
+// spin limit of 0 makes every wait give up at its first poll, complete or
+// not (the host sets it only to test this path); the kernel still drains.
 __device__ __forceinline__ bool keep_waiting(unsigned* spins, DevState* st) {
+  const unsigned lim = st->spin_limit;
   __builtin_amdgcn_s_sleep(2);
   ++*spins;
-  if ((*spins & 255u) == 0u &&
-      (*spins > kSpinLimit ||
+  if (*spins > lim ||
+      ((*spins & 255u) == 0u &&
        __hip_atomic_load(&st->barrier_err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)) {
     __hip_atomic_store(&st->barrier_err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return false;
   }
   return true;
+}
+
+// Whether this launch's waits are forced to give up (read once per kernel).
+__device__ __forceinline__ bool waits_forced(const DevState* st) {
+  return st->spin_limit == 0u;
 }
 
 }  // namespace

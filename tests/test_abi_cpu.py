@@ -43,11 +43,14 @@ def test_workspace_size_host_only():
     assert lib.rrf_workspace_size(1, 16384, 16384, 64, 0, ctypes.byref(out)) == 0
     # Bws alone is 16384^2 doubles.
     assert out.value >= 16384 * 16384 * 8 * 3
+    # Blocks of up to 128 columns (run as 64-column sub-blocks).
+    assert lib.rrf_workspace_size(1, 100, 50, 128, 0, ctypes.byref(out)) == 0
+    assert lib.rrf_workspace_size(1, 16384, 16384, 64, 0, ctypes.byref(out)) == 0
     small = ctypes.c_size_t()
     assert lib.rrf_workspace_size(0, 100, 50, 16, 10, ctypes.byref(small)) == 0
     assert 0 < small.value < out.value
     for bad in [(2, 10, 10, 8, 0), (1, 0, 10, 8, 0), (1, 10, 10, 0, 0),
-                (1, 10, 10, 65, 0), (1, 10, 10, 8, -1)]:
+                (1, 10, 10, 129, 0), (1, 10, 10, 8, -1)]:
         assert lib.rrf_workspace_size(*bad, ctypes.byref(out)) == _abi.RRF_ERR_INVALID_ARG
     assert lib.rrf_workspace_size(1, 10, 10, 8, 0, None) == _abi.RRF_ERR_INVALID_ARG
 
@@ -59,7 +62,7 @@ def test_invalid_arguments_rejected_before_device():
     assert lib.rrf_plan_create(None, 1, 10, 10, 8, 0, None) == E
     assert lib.rrf_plan_create(ctypes.byref(h), 7, 10, 10, 8, 0, None) == E
     assert lib.rrf_plan_create(ctypes.byref(h), 1, 0, 10, 8, 0, None) == E
-    assert lib.rrf_plan_create(ctypes.byref(h), 1, 10, 10, 65, 0, None) == E
+    assert lib.rrf_plan_create(ctypes.byref(h), 1, 10, 10, 129, 0, None) == E
     q, b = ctypes.c_void_p(), ctypes.c_void_p()
     l1, l2, k = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64(7)
     assert lib.rrf_run(None, ctypes.c_void_p(8), 4, 4, 4, 0.1, 2, 1,

@@ -42,8 +42,32 @@ def _run(A, w, k_max=0, stop=rrf.RRF_STOP_TRAILING):
         return to_host(Q), to_host(B), k, tr, st
 
 
+_ORACLE = {}
+
+
+def _oracle(w, A, k_max=0, stop="trailing"):
+    """The oracle's result for workload w (cached: several GPU variants of the
+    same workload compare with one oracle run)."""
+    key = (w, k_max, stop)
+    if key not in _ORACLE:
+        _ORACLE[key] = oracle.hbarrf(A, w.tol, w.block_b, w.sketch_seed, k_max=k_max,
+                                     dtype=w.np_dtype, stop=stop)
+    return _ORACLE[key]
+
+
+def _elementwise_bound(A, k, w):
+    """Q is unique given Omega (Theorem 3.1 + the sign convention); its
+    columns agree with the oracle's to about cond(A Omega_k) u, and B's
+    entries to that times ||A||_2."""
+    dt = np.dtype(w.dtype)
+    Om = oracle.normal_v1(w.sketch_seed, A.shape[1], 0, k, dtype=dt).astype(np.float64)
+    sv = np.linalg.svd(A.astype(np.float64) @ Om, compute_uv=False)
+    tol = 1e3 * (sv[0] / sv[-1]) * np.finfo(dt).eps
+    return tol, tol * np.linalg.norm(A.astype(np.float64), 2)
+
+
 def _check_against_live_oracle(w, A, gap=False, elementwise=False):
-    ref = oracle.hbarrf(A, w.tol, w.block_b, w.sketch_seed, dtype=w.np_dtype)
+    ref = _oracle(w, A)
     say(f"run {w.name} m={w.m} n={w.n} b={w.block_b} tol={w.tol} oracle k={ref.k}")
     Q, B, k, tr, _ = _run(A, w)
     assert k == ref.k
@@ -58,14 +82,9 @@ def _check_against_live_oracle(w, A, gap=False, elementwise=False):
     if gap and k > 0:
         assert projector_distance(Q, ref.Q) <= PROJ_TOL[dt]
     if elementwise and k > 0:
-        # Q is unique given Omega (Theorem 3.1 + the sign convention); its
-        # columns agree to about cond(A Omega) * u.
-        Om = oracle.normal_v1(w.sketch_seed, A.shape[1], 0, k, dtype=dt).astype(np.float64)
-        sv = np.linalg.svd(A.astype(np.float64) @ Om, compute_uv=False)
-        cond = sv[0] / sv[-1]
-        tol = 1e3 * cond * np.finfo(dt).eps
-        assert np.max(np.abs(Q - ref.Q)) <= tol
-        assert np.max(np.abs(B - ref.B)) <= tol * np.linalg.norm(A, 2)
+        tq, tb = _elementwise_bound(A, k, w)
+        assert np.max(np.abs(Q - ref.Q)) <= tq
+        assert np.max(np.abs(B - ref.B)) <= tb
     return Q, B, k, ref
 
 
@@ -86,8 +105,11 @@ SCALED = [
 
 @pytest.mark.parametrize("name,m,n,b,tol", SCALED)
 def test_scaled_workloads(name, m, n, b, tol):
+    # Element by element: with b = 64 and 48 this is the look-ahead path
+    # (update_panel_kernel with its fused sample, the redundant panel update
+    # in thin_apply_kernel, block 0's panel beside the first sample).
     w = W.scaled(name, m, n, block_b=b, tol=tol)
-    _check_against_live_oracle(w, W.build_matrix(w))
+    _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
 
 
 @pytest.mark.parametrize("name,m,n,b,tol", [SCALED[0], SCALED[2], SCALED[3], SCALED[5]])
@@ -104,7 +126,7 @@ def test_scaled_workloads_without_lookahead(monkeypatch, name, m, n, b, tol):
     # launch, no redundant panel update, no block-0 sample/panel launch).
     monkeypatch.setenv("RRF_LOOKAHEAD", "0")
     w = W.scaled(name, m, n, block_b=b, tol=tol)
-    _check_against_live_oracle(w, W.build_matrix(w))
+    _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
 
 
 @pytest.mark.parametrize("name,m,n,b,tol", SCALED)
@@ -169,6 +191,92 @@ def test_subtract_mode_matches_oracle():
     assert k == ref.k
     for (_, _, e_s), g in zip(ref.trace, tr["E_sub"]):
         assert abs(g - e_s) <= 1e-9 * ref.E0
+
+
+@pytest.mark.parametrize("lookahead", ["1", "0"])
+def test_lookahead_tall_panel_elementwise(monkeypatch, lookahead):
+    # 12288 rows at b = 64: the panel inside the look-ahead launch holds 64
+    # rows per thread (panels above 8192 rows); k = 320 in five blocks,
+    # E / sigma^2 = 3.0 at k = 256 and 0.17 at 320.
+    monkeypatch.setenv("RRF_LOOKAHEAD", lookahead)
+    w = W.scaled("square_fp64_16384", 12288, 384, block_b=64, tol=1e-2)
+    _, _, k, _ = _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
+    assert k == 320
+
+
+@pytest.mark.parametrize("name,m,n,b,tol", [
+    ("square_fp64_16384", 2048, 2048, 128, 1e-5),    # two 64-column sub-blocks
+    ("tiny_fp64_500x300", 333, 250, 100, 1e-5),      # sub-blocks of 64 and 36
+    ("galore_fp32_4096x4096", 1024, 1024, 80, 2e-2), # 64 and 16: mixed panel routes
+])
+def test_blocks_wider_than_64(name, m, n, b, tol):
+    # block_b > 64 runs as sub-blocks of at most 64 columns with the stop
+    # test at block ends; the oracle factors each block whole.
+    w = W.scaled(name, m, n, block_b=b, tol=tol)
+    _, _, k, ref = _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
+    assert k % b == 0 or k == min(m, n)
+
+
+def test_panel_beyond_register_capacity():
+    # 131072 rows at b = 64: no register-resident panel grid holds the panel,
+    # so it takes the tall-skinny QR tree.  Fixed rank k = 128 (tol = 0,
+    # k_cap = n); the oracle is the plain definition of the result
+    # (Theorem 3.1): the Householder QR of A Omega_k (the oracle's geqr2 and
+    # org2r) and B = Q^T A.
+    w = W.scaled("tall_fp64_131072x2048", 131072, 128, block_b=64, tol=0.0)
+    A = W.build_matrix(w)
+    say("tall 131072x128 b=64: oracle plain definition")
+    Om = oracle.normal_v1(w.sketch_seed, 128, 0, 128, dtype=np.float64)
+    Vo, tauo = oracle.geqr2(A @ Om)
+    Qo = oracle.org2r(Vo, tauo)
+    Bo = Qo.T @ A
+    say("tall 131072x128 b=64: rrf_run")
+    Q, B, k, _, st = _run(A, w)
+    assert k == 128 and st == rrf.RRF_OK
+    tq, tb = _elementwise_bound(A, k, w)
+    assert np.max(np.abs(Q - Qo)) <= tq
+    assert np.max(np.abs(B - Bo)) <= tb
+    assert orth_err(Q) <= ORTH_TOL[np.dtype(np.float64)]
+
+
+def test_deterministic_repeat_lookahead():
+    # Bit-identical results from two runs of the look-ahead path (b = 64).
+    w = W.scaled("square_fp64_16384", 2048, 2048, tol=1e-5)
+    A = to_dev(W.build_matrix(w))
+    with rrf.Plan(torch.float64, 2048, 2048, 64) as p:
+        Q1, B1, k1 = p.run(A, w.tol, 64, w.sketch_seed)
+        Q2, B2, k2 = p.run(A, w.tol, 64, w.sketch_seed)
+        torch.cuda.synchronize()
+        assert k1 == k2 and k1 > 64
+        assert torch.equal(Q1, Q2) and torch.equal(B1, B2)
+
+
+def test_wait_give_up_is_reported(monkeypatch):
+    # A spin limit of 0 (set from the host) makes every grid-wide wait give
+    # up at its first poll; each kernel still runs to its end.  The run and
+    # the stage entry points must report RRF_ERR_INTERNAL, and a plan with the
+    # default limit must work afterwards.
+    monkeypatch.setenv("RRF_TEST_SPIN_LIMIT", "0")
+    w = W.scaled("square_fp64_16384", 1024, 1024, tol=1e-5)
+    A = W.build_matrix(w)
+    Ad = to_dev(A)
+    say("wait give-up: rrf_run, rrf_panel_qr, thin rrf_apply_block_reflector")
+    with rrf.Plan(torch.float64, 1024, 1024, 64) as p:
+        with pytest.raises(rrf.RRFError) as e:
+            p.run(Ad, w.tol, 64, w.sketch_seed)
+        assert e.value.status == -6
+        Y = to_dev(W.random_dense(1024, 64, np.float64, 3))
+        with pytest.raises(rrf.RRFError) as e:
+            p.panel_qr(Y)
+        assert e.value.status == -6
+        Vt = to_dev(oracle.geqr2(W.random_dense(1024, 32, np.float64, 4))[0])
+        Tt = to_dev(np.triu(W.random_dense(32, 32, np.float64, 5)))
+        X = to_dev(W.random_dense(1024, 8, np.float64, 6))
+        with pytest.raises(rrf.RRFError) as e:
+            p.apply_block_reflector(Vt, Tt, X)
+        assert e.value.status == -6
+    monkeypatch.delenv("RRF_TEST_SPIN_LIMIT")
+    _check_against_live_oracle(w, A)
 
 
 def test_deterministic_repeat():
