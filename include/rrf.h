@@ -229,6 +229,34 @@ rrf_status rrf_subspace_map(rrf_plan_t plan, const void* Qnew, int64_t ldqn,
                             int64_t r_old, const void* M, int64_t ldm,
                             int64_t m, int64_t n, void* out, int64_t ldo);
 
+/* ---------------------------------------------------------------------------
+ * rrf_panel_qr_noalloc -- rrf_panel_qr for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): no plan, and no hipMalloc, hipFree or
+ * allocating library call.  The panel runs the column-by-column route of
+ * rrf_panel_qr (same V, tau and T semantics: LAPACK geqrt, dlarfg sign
+ * convention, V unit lower trapezoidal with explicit ones and zeros, T upper
+ * triangular with its lower part zeroed).
+ *   dtype        RRF_F32 or RRF_F64 (element type of Y, V, T, tau).
+ *   Y            device, m x b (ldy >= m), read only.
+ *   V, T, tau    device outputs: m x b (ldv >= m), b x b (ldt >= b), b.
+ *   wait_status  device int or NULL; receives 0, or 1 if a grid-wide wait
+ *                gave up (outputs then undefined).
+ *   hip_stream   hipStream_t (NULL: the null stream); the call is
+ *                asynchronous on it.
+ * Limits: 1 <= b <= 64, b <= m <= 16384 (RRF_ERR_SHAPE above).  Its scratch
+ * (gathered panel, V and T staging, exchange words, wait flag; about 16.7
+ * MiB) is one static device array per GPU, set up on the first call on that
+ * device and held until the process ends.  Every call on a GPU shares that
+ * array: calls that overlap on one GPU (several streams) race.
+ * Errors: RRF_ERR_INVALID_ARG (checked on the host before any device call),
+ * RRF_ERR_SHAPE, RRF_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+rrf_status rrf_panel_qr_noalloc(rrf_dtype dtype, const void* Y, int64_t m,
+                                int64_t b, int64_t ldy, void* V, int64_t ldv,
+                                void* T, int64_t ldt, void* tau,
+                                int* wait_status, void* hip_stream);
+
 /* dst[r + c*ldd] = src[r + c*lds] for r < rows, c < cols (device to device,
  * asynchronous on hip_stream). */
 rrf_status rrf_copy_matrix(rrf_dtype dtype, const void* src, int64_t lds,

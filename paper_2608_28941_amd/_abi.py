@@ -52,6 +52,8 @@ SIGNATURES = {
     "rrf_apply_block_reflector": (_int, [_vp, _int, _vp, _i64, _vp, _i64, _i64,
                                          _vp, _i64, _i64, _i64]),
     "rrf_copy_matrix": (_int, [_int, _vp, _i64, _vp, _i64, _i64, _i64, _vp]),
+    "rrf_panel_qr_noalloc": (_int, [_int, _vp, _i64, _i64, _i64, _vp, _i64, _vp, _i64,
+                                    _vp, _vp, _vp]),
     "rrf_subspace_map": (_int, [_vp, _vp, _i64, _i64, _vp, _i64, _i64, _vp, _i64,
                                 _i64, _i64, _vp, _i64]),
 }

@@ -40,9 +40,6 @@ constexpr int kPanelTsqr = 1;      // tall-skinny QR + Householder reconstructio
 constexpr int kPanelGram = 2;      // column recurrence from the Gram matrix, one exchange per sweep
 constexpr int kPanelAuto = 3;      // kPanelGram for blocks of <= 32 columns, else kPanelGrid
 constexpr int kTLd = 64;          // T stored like geqrt's T: 64 rows
-// Poll rounds before a grid-wide wait gives up (each a short sleep plus a
-// trip to the coherent memory path: tens of seconds in all).
-constexpr unsigned kSpinLimit = 1u << 24;
 
 struct Sizes {
   int64_t ldb, kcap, kcols;

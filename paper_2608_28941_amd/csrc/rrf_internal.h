@@ -21,6 +21,10 @@ constexpr int kRedChunk = 64;      // granularity of the reduce's row splits
 constexpr int kPanelThreads = 256;
 constexpr int kMaxPanelWGs = 1024;
 
+// Poll rounds before a grid-wide wait gives up (each a short sleep plus a
+// trip to the coherent memory path: tens of seconds in all).
+constexpr unsigned kSpinLimit = 1u << 24;
+
 inline int pad16(int64_t b) { return b <= 16 ? 16 : (b <= 32 ? 32 : 64); }
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }

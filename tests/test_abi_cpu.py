@@ -84,6 +84,15 @@ def test_invalid_arguments_rejected_before_device():
                                          4, 4) == E
     assert lib.rrf_subspace_map(None, ctypes.c_void_p(8), 4, 2, ctypes.c_void_p(8), 4, 2,
                                 ctypes.c_void_p(8), 2, 4, 3, ctypes.c_void_p(8), 2) == E
+    p8 = ctypes.c_void_p(8)
+    assert lib.rrf_panel_qr_noalloc(1, None, 100, 8, 100, p8, 100, p8, 8, p8, None,
+                                    None) == E
+    assert lib.rrf_panel_qr_noalloc(3, p8, 100, 8, 100, p8, 100, p8, 8, p8, None, None) == E
+    assert lib.rrf_panel_qr_noalloc(1, p8, 100, 8, 100, p8, 100, p8, 7, p8, None, None) == E
+    assert lib.rrf_panel_qr_noalloc(1, p8, 7, 8, 100, p8, 100, p8, 8, p8, None, None) == E
+    # Beyond the static scratch: rejected before any device call.
+    assert lib.rrf_panel_qr_noalloc(1, p8, 20000, 8, 20000, p8, 20000, p8, 8, p8, None,
+                                    None) == _abi.RRF_ERR_SHAPE
 
 
 def test_plan_create_without_gpu_reports_hip_error():
