@@ -13,7 +13,11 @@ Based on an Implicit Householder QR Decomposition"):
                      (the paper only asks for standard Gaussian entries,
                      Alg. 2, sketch step).
 * ``hbarrf``      -- Alg. 2 step by step, with unblocked Householder
-                     reflections (geqr2 semantics), in float64.
+                     reflections (geqr2 semantics), in float64; optionally
+                     with the spectral-norm stopping test and the power
+                     iterations the conclusion proposes.
+* ``spectral_estimate`` -- the estimate of the spectral norm of the rows not
+                     yet in B that the spectral stopping test uses.
 * ``stability``   -- the Sec. 6 stability experiment (Fig. 3) in fp32:
                      Alg. 2 against block Gram-Schmidt (Alg. 1) with and
                      without reorthogonalisation (``python -m oracle.stability``).
@@ -34,6 +38,7 @@ from .range_finder import (
     larft,
     org2r,
     frob2,
+    spectral_estimate,
 )
 from .subspace import subspace_map
 
@@ -48,5 +53,6 @@ __all__ = [
     "larft",
     "org2r",
     "frob2",
+    "spectral_estimate",
     "subspace_map",
 ]

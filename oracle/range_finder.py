@@ -26,6 +26,15 @@ the paper that this file takes (all listed in the design doc as well):
   tau = (beta - alpha) / beta, tau = 0 when x[1:] = 0).
 * Precision: inputs (A and the sketch) are first rounded to the working dtype
   of the configuration, then everything is computed in float64.
+* Spectral stopping (``stop="spectral"``; the alternative Sec. 3 mentions
+  and the conclusion leaves to future work): the spectral norm of the rows
+  not yet in B is estimated after each block by ``spectral_estimate`` on the
+  next sketch block (its first min(b, 64) columns), and the loop stops once
+  the estimate is <= sigma^2 (sigma = tol ||A||_F, as in the other modes).
+* Power iterations (``power=q``; the conclusion's proposal for slowly
+  decaying spectra, A replaced by (A A^T)^q A): each block's sample is
+  (B B^T)^q B Omega_i on the rows not yet in B, with no orthonormalisation
+  between the products.
 """
 
 from dataclasses import dataclass, field
@@ -141,6 +150,24 @@ def org2r(V, tau):
     return Q
 
 
+def spectral_estimate(Bt, Om):
+    """Estimate of ||Bt||_2^2 from a Gaussian block Om: the largest squared
+    norm of Bt^T x over unit x in span(Bt Om), i.e. ||P Bt||_2^2 with P the
+    orthogonal projector onto that span (one step of randomized subspace
+    iteration; a lower bound of ||Bt||_2^2, exact when rank(Bt) <= the
+    block width).  The span is taken from an SVD of Y = Bt Om, dropping
+    directions below the roundoff of Y."""
+    Bt = np.asarray(Bt, dtype=np.float64)
+    if Bt.size == 0 or Om.shape[1] == 0:
+        return 0.0
+    Y = Bt @ Om
+    U, sv, _ = np.linalg.svd(Y, full_matrices=False)
+    if sv.size == 0 or sv[0] == 0.0:
+        return 0.0
+    r = int(np.count_nonzero(sv > sv[0] * max(Y.shape) * np.finfo(np.float64).eps))
+    return float(np.linalg.norm(U[:, :r].T @ Bt, 2) ** 2)
+
+
 @dataclass
 class HbarrfResult:
     k: int
@@ -156,7 +183,7 @@ class HbarrfResult:
     extras: dict = field(default_factory=dict)
 
 
-def hbarrf(A, tol, block_b, seed, k_max=0, dtype=None, stop="trailing"):
+def hbarrf(A, tol, block_b, seed, k_max=0, dtype=None, stop="trailing", power=0):
     """Alg. 2: blocked adaptive range finder on an implicit Householder QR.
 
     A        m x n input (its values are used as given; pass A already rounded
@@ -167,7 +194,10 @@ def hbarrf(A, tol, block_b, seed, k_max=0, dtype=None, stop="trailing"):
     k_max    rank cap; 0 means min(m, n)  (also the fixed-rank mode of Sec. 6)
     dtype    working dtype of the sketch (float32 sketches are the float64
              sketch rounded to nearest-even); default A's dtype
-    stop     "trailing" (default) or "subtract" (the paper's running difference)
+    stop     "trailing" (default), "subtract" (the paper's running
+             difference) or "spectral" (estimated spectral norm of the rows
+             not yet in B, ``spectral_estimate``)
+    power    power iterations per block sample (0: Alg. 2 as printed)
     """
     A = np.asarray(A)
     if A.ndim != 2:
@@ -179,8 +209,10 @@ def hbarrf(A, tol, block_b, seed, k_max=0, dtype=None, stop="trailing"):
         raise ValueError("tol must be finite and >= 0")
     if block_b < 1 or k_max < 0:
         raise ValueError("block_b must be >= 1 and k_max >= 0")
-    if stop not in ("trailing", "subtract"):
-        raise ValueError("stop must be 'trailing' or 'subtract'")
+    if stop not in ("trailing", "subtract", "spectral"):
+        raise ValueError("stop must be 'trailing', 'subtract' or 'spectral'")
+    if power < 0:
+        raise ValueError("power must be >= 0")
     m, n = A.shape
 
     # Alg. 2 initialisation: E <- ||A||_F^2, B <- A, V <- 0, i <- 0.
@@ -196,18 +228,22 @@ def hbarrf(A, tol, block_b, seed, k_max=0, dtype=None, stop="trailing"):
     trace = []
     E_trail = E0
     E_sub = E0
+    E_spec = E0      # before any block the test falls back on ||A||_F^2
     k = 0
 
     def current_E():
-        return E_trail if stop == "trailing" else E_sub
+        return {"trailing": E_trail, "subtract": E_sub, "spectral": E_spec}[stop]
 
     # Alg. 2 loop: while E > sigma^2 (and ranks remain, Sec. 4 termination).
     while current_E() > sigma2 and k < k_cap:
         bi = min(block_b, k_cap - k)
         # Fresh Gaussian block: global sketch columns [k, k + bi).
         Om = normal_v1(seed, n, k, bi, dtype=dtype).astype(np.float64)
-        # (V_i, T_i) <- qr(B_{i:j} Omega)  -- sample the not-yet-final rows.
+        # (V_i, T_i) <- qr(B_{i:j} Omega)  -- sample the not-yet-final rows,
+        # optionally (B B^T)^q B Omega.
         Y = Bw[k:, :] @ Om
+        for _ in range(power):
+            Y = Bw[k:, :] @ (Bw[k:, :].T @ Y)
         Vi, ti = geqr2(Y)
         V[k:, k:k + bi] = Vi
         tau[k:k + bi] = ti
@@ -218,10 +254,22 @@ def hbarrf(A, tol, block_b, seed, k_max=0, dtype=None, stop="trailing"):
         E_sub = max(0.0, E_sub - frob2(Bw[k:k + bi, :]))
         E_trail = frob2(Bw[k + bi:, :])
         k += bi
-        trace.append((k, E_trail, E_sub))
+        if stop == "spectral":
+            # On the next sketch block's first min(b, 64) columns.
+            p = min(block_b, 64, k_cap - k)
+            if p > 0:
+                On = normal_v1(seed, n, k, p, dtype=dtype).astype(np.float64)
+                E_spec = spectral_estimate(Bw[k:, :], On)
+            else:
+                E_spec = float("nan")
+        trace.append((k, E_trail, E_sub) if stop != "spectral"
+                     else (k, E_trail, E_sub, E_spec))
 
     status = STATUS_OK
-    if current_E() > sigma2 and k == k_cap and k_cap < min(m, n):
+    # At the cap the spectral estimate is not formed; the Frobenius norm (an
+    # upper bound of the spectral norm) decides the warning there.
+    E_end = E_trail if stop == "spectral" else current_E()
+    if E_end > sigma2 and k == k_cap and k_cap < min(m, n):
         status = STATUS_WARN_KMAX
     Q = org2r(V[:, :k], tau[:k])
     B = np.array(Bw[:k, :], order="F", copy=True)
