@@ -57,10 +57,21 @@ typedef enum rrf_status {
   RRF_ERR_INTERNAL = -6      /* a device-side bounded wait gave up             */
 } rrf_status;
 
-/* Stopping quantity (Alg. 2, E update; Sec. 6 discussion of cancellation). */
+/* Stopping quantity (Alg. 2, E update; Sec. 6 discussion of cancellation;
+ * the spectral-norm alternative of Sec. 3, left to future work in the
+ * conclusion).  The loop stops once E <= sigma^2, sigma = tol ||A||_F. */
 typedef enum rrf_stop_mode {
   RRF_STOP_TRAILING = 0,     /* E = ||B[k:m, :]||_F^2 computed directly (default) */
-  RRF_STOP_SUBTRACT = 1      /* E = ||A||_F^2 - sum_i ||B_i||_F^2, clamped >= 0  */
+  RRF_STOP_SUBTRACT = 1,     /* E = ||A||_F^2 - sum_i ||B_i||_F^2, clamped >= 0  */
+  RRF_STOP_SPECTRAL = 2      /* E = estimate of ||B[k:m, :]||_2^2: with Y the     */
+                             /* next sketch block's first min(b, 64) columns    */
+                             /* sampled from B[k:m, :] and Z = B[k:m, :]^T Y,  */
+                             /* the largest eigenvalue of (Z^T Z, Y^T Y), i.e.  */
+                             /* max ||B^T x||^2 / ||x||^2 over x in span(Y): a  */
+                             /* lower bound, exact when the trailing rank fits  */
+                             /* the block.  One more pass over B[k:m, :] per    */
+                             /* block.  At the rank cap the Frobenius norm      */
+                             /* decides RRF_WARN_KMAX.                          */
 } rrf_stop_mode;
 
 /* Stages reported by rrf_get_stage_stats. */
@@ -112,7 +123,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
  *             A must be ready on the plan's stream.
  *   tol       relative Frobenius tolerance, finite, >= 0; sigma = tol ||A||_F.
  *             tol >= 1 or A = 0 gives k = 0.
- *   block_b   1 <= block_b <= block_b_max.
+ *   block_b   1 <= block_b <= block_b_max (<= 64 with power iterations).
  *   seed      sketch seed (RRF-NORMAL-v1, domain 0): Omega_i is columns
  *             [i b, i b + b_i) of one global n x inf Gaussian matrix.
  * Outputs (plan-owned device memory, valid until the next rrf_run on this
@@ -144,15 +155,27 @@ rrf_status rrf_workspace_size(rrf_dtype dtype, int64_t m_max, int64_t n_max,
 /* Select the stopping quantity for later runs (default RRF_STOP_TRAILING). */
 rrf_status rrf_set_stop_mode(rrf_plan_t plan, rrf_stop_mode mode);
 
+/* Power iterations for later runs (the conclusion's proposal for slowly
+ * decaying spectra, A replaced by (A A^T)^q A): each block's sample becomes
+ * (B B^T)^q B Omega_i on the rows of B not yet final, without
+ * orthonormalisation between the products (two more passes over those rows
+ * per iteration; the look-ahead is off).  0 <= q <= 8; default 0.  With
+ * q > 0, rrf_run requires block_b <= 64 (RRF_ERR_INVALID_ARG otherwise: a
+ * wider block runs as 64-column sub-blocks, and powers taken per sub-block
+ * would act on the partly deflated matrix). */
+rrf_status rrf_set_power_iterations(rrf_plan_t plan, int q);
+
 /* Enable (1) or disable (0) per-kernel HIP-event timing for later runs. */
 rrf_status rrf_set_timing(rrf_plan_t plan, int enable);
 
 /* Per-block trace of the last run, host arrays of length >= cap:
- * E_trail[i], E_sub[i] after block i; *E0 = ||A||_F^2, *sigma2 = (tol ||A||_F)^2.
+ * E_trail[i], E_sub[i] after block i, E_spec[i] the spectral estimate after
+ * block i (spectral mode, blocks that ended below the cap; NaN otherwise;
+ * E_spec may be NULL); *E0 = ||A||_F^2, *sigma2 = (tol ||A||_F)^2.
  * *nblocks = number of blocks run (min with cap values written). */
 rrf_status rrf_get_trace(rrf_plan_t plan, int64_t cap, int64_t* nblocks,
-                         double* E_trail, double* E_sub, double* E0,
-                         double* sigma2);
+                         double* E_trail, double* E_sub, double* E_spec,
+                         double* E0, double* sigma2);
 
 /* Per-stage statistics of the last run, host arrays of length RRF_NUM_STAGES:
  * ms[s]       summed kernel time (HIP events; 0 unless timing was enabled),

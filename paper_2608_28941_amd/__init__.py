@@ -15,10 +15,10 @@ import ctypes
 
 from . import _abi
 from ._abi import (RRFError, RRF_F32, RRF_F64, RRF_OK, RRF_WARN_KMAX,
-                   RRF_STOP_TRAILING, RRF_STOP_SUBTRACT, STAGES)
+                   RRF_STOP_TRAILING, RRF_STOP_SUBTRACT, RRF_STOP_SPECTRAL, STAGES)
 
 __all__ = ["Plan", "run", "sketch", "colmajor", "RRFError", "STAGES",
-           "RRF_STOP_TRAILING", "RRF_STOP_SUBTRACT"]
+           "RRF_STOP_TRAILING", "RRF_STOP_SUBTRACT", "RRF_STOP_SPECTRAL"]
 
 
 def _torch():
@@ -106,6 +106,10 @@ class Plan:
         _abi.check(self.lib.rrf_set_stop_mode(self.handle, int(mode)),
                    "rrf_set_stop_mode")
 
+    def set_power_iterations(self, q):
+        _abi.check(self.lib.rrf_set_power_iterations(self.handle, int(q)),
+                   "rrf_set_power_iterations")
+
     def set_timing(self, enable):
         _abi.check(self.lib.rrf_set_timing(self.handle, 1 if enable else 0),
                    "rrf_set_timing")
@@ -150,21 +154,25 @@ class Plan:
         return Q, B, k
 
     def trace(self):
-        """Per-block (E_trail, E_sub) of the last run, plus E0 and sigma^2."""
+        """Per-block (E_trail, E_sub, E_spec) of the last run, plus E0 and
+        sigma^2."""
         nb = ctypes.c_int64()
         e0 = ctypes.c_double()
         s2 = ctypes.c_double()
         _abi.check(self.lib.rrf_get_trace(self.handle, 0, ctypes.byref(nb), None,
-                                          None, ctypes.byref(e0), ctypes.byref(s2)),
+                                          None, None, ctypes.byref(e0),
+                                          ctypes.byref(s2)),
                    "rrf_get_trace")
         cap = nb.value
         et = (ctypes.c_double * max(cap, 1))()
         es = (ctypes.c_double * max(cap, 1))()
+        ep = (ctypes.c_double * max(cap, 1))()
         _abi.check(self.lib.rrf_get_trace(self.handle, cap, ctypes.byref(nb), et,
-                                          es, ctypes.byref(e0), ctypes.byref(s2)),
+                                          es, ep, ctypes.byref(e0), ctypes.byref(s2)),
                    "rrf_get_trace")
         return {"E_trail": list(et)[:cap], "E_sub": list(es)[:cap],
-                "E0": e0.value, "sigma2": s2.value, "nblocks": cap}
+                "E_spec": list(ep)[:cap], "E0": e0.value, "sigma2": s2.value,
+                "nblocks": cap}
 
     def stage_stats(self):
         n = _abi.RRF_NUM_STAGES
@@ -243,13 +251,16 @@ class Plan:
         return out
 
 
-def run(A, tol, block_b, seed, k_max=0, stop_mode=RRF_STOP_TRAILING):
-    """One-shot range finder: (Q, B, k) with ||A - Q B||_F <= tol ||A||_F."""
+def run(A, tol, block_b, seed, k_max=0, stop_mode=RRF_STOP_TRAILING, power=0):
+    """One-shot range finder: (Q, B, k) with ||A - Q B||_F <= tol ||A||_F
+    (spectral mode: the estimated spectral norm of the residual <= tol
+    ||A||_F)."""
     A = colmajor(A)
     m, n = A.shape
     with Plan(A.dtype, max(m, 1), max(n, 1), block_b, k_max,
               device=A.device) as p:
         p.set_stop_mode(stop_mode)
+        p.set_power_iterations(power)
         return p.run(A, tol, block_b, seed)
 
 

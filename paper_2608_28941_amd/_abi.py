@@ -19,7 +19,7 @@ RRF_ERR_NONFINITE = -3
 RRF_ERR_NOMEM = -4
 RRF_ERR_HIP = -5
 RRF_ERR_INTERNAL = -6
-RRF_STOP_TRAILING, RRF_STOP_SUBTRACT = 0, 1
+RRF_STOP_TRAILING, RRF_STOP_SUBTRACT, RRF_STOP_SPECTRAL = 0, 1, 2
 STAGES = ["sketch", "sample", "panel", "reduce", "formw", "update",
           "finalize", "orgqr"]
 RRF_NUM_STAGES = len(STAGES)
@@ -43,7 +43,8 @@ SIGNATURES = {
                                   ctypes.POINTER(ctypes.c_size_t)]),
     "rrf_set_stop_mode": (_int, [_vp, _int]),
     "rrf_set_timing": (_int, [_vp, _int]),
-    "rrf_get_trace": (_int, [_vp, _i64, _pi64, _pd, _pd, _pd, _pd]),
+    "rrf_get_trace": (_int, [_vp, _i64, _pi64, _pd, _pd, _pd, _pd, _pd]),
+    "rrf_set_power_iterations": (_int, [_vp, _int]),
     "rrf_get_stage_stats": (_int, [_vp, _pd, _pi64, _pd, _pd]),
     "rrf_get_reflectors": (_int, [_vp, _pvp, _pi64, _pvp, _pi64, _pvp]),
     "rrf_sketch": (_int, [_int, _u64, _i64, _i64, _i64, _vp, _i64, _vp]),

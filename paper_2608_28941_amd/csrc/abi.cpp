@@ -45,10 +45,10 @@ struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
-      rowj, st, trace, tsqr, gx, tx;
+      rowj, st, trace, tsqr, gx, tx, Yest, spec, Tpow;
   size_t total() const {
     return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
-           normpart + red + rowj + st + trace + tsqr + gx + tx;
+           normpart + red + rowj + st + trace + tsqr + gx + tx + Yest + spec + Tpow;
   }
 };
 
@@ -81,7 +81,12 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.gx = (size_t)(kGramPartWords + kGramSumWords) * 8;
   z.tx = (size_t)(kThinPartWords + kThinSumWords) * 8;
   z.st = sizeof(DevState);
-  z.trace = (size_t)2 * std::max<int64_t>(z.kcap, 1) * 8;
+  z.trace = (size_t)3 * std::max<int64_t>(z.kcap, 1) * 8;
+  // Spectral-norm estimate: the gathered next sample, the Gram partials;
+  // power iterations: their scaled identity.
+  z.Yest = (size_t)z.ldysum * 64 * 8;
+  z.spec = (size_t)kMaxSpecWGs * 4096 * 8;
+  z.Tpow = (size_t)64 * 64 * 8;
   // Tall-skinny QR panel: the largest tree over the block widths the plan
   // allows (the tree shrinks with the panel's rows).
   z.tsqr = 8;
@@ -115,7 +120,9 @@ struct rrf_plan {
   double* tsqr;              // scratch of the tall-skinny QR panel
   int panel_mode;            // kPanelGrid, kPanelTsqr, kPanelGram or kPanelAuto
   double *V, *Tm, *tau, *Ysum;
-  double *normpart, *trace_trail_d, *trace_sub_d;
+  double *normpart, *trace_trail_d, *trace_sub_d, *trace_spec_d;
+  double *Yest, *spec_part, *Tpow;
+  int power;                 // power iterations per block sample
   unsigned long long *red, *rowj, *gx, *tx;
   DevState* st;
   DevState* st_host;
@@ -125,7 +132,7 @@ struct rrf_plan {
   // last run
   int64_t last_m, last_n, last_k, last_b, nblocks;
   double E0, sigma2;
-  std::vector<double> trace_trail, trace_sub;
+  std::vector<double> trace_trail, trace_sub, trace_spec;
   std::vector<int64_t> sub_start;   // first column of each sub-block of the last run
   std::vector<SpecWork> spec;       // speculative credits of the last run
   double ms[RRF_NUM_STAGES], flops[RRF_NUM_STAGES], bytes[RRF_NUM_STAGES];
@@ -454,6 +461,9 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   hipError_t he = read_state(p);
   if (he != hipSuccess) return hip_fail(he);
   if (p->st_host->nonfinite) return RRF_ERR_NONFINITE;
+  const int power = p->power;
+  if (power > 0)
+    RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 0.0, 0.0, launch_scaled_identity(p->Tpow, 64, p->st, s));
 
   // Look-ahead (the paper's two-queue overlap, Sec. 5, on one GPU): the
   // update of sub-block i samples Omega_{i+2} instead of Omega_{i+1}; the
@@ -464,7 +474,9 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   // few workgroups of the update's own launch while the rest update B.
   // It pays when the panel grid is small: a panel of more than a quarter of
   // the compute units takes too many slots from the update it runs beside.
-  bool la = p->lookahead != 0 && panel_alg(p, b0) == kPanelGrid && kcap > b0;
+  // Power iterations need the whole updated trailing matrix before the
+  // sample, so they run without it.
+  bool la = p->lookahead != 0 && power == 0 && panel_alg(p, b0) == kPanelGrid && kcap > b0;
   if (la) {
     PanelShape sh1;
     la = panel_shape(m - b0, (int)sub_width(b0), p->num_cus, p->panel_target, &sh1) &&
@@ -509,6 +521,81 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   };
   auto panel_flops = [](double mr, double bb) {
     return 2.0 * mr * bb * bb - 2.0 / 3.0 * bb * bb * bb + 1.0 * mr * bb * bb;
+  };
+  // Power iterations (the conclusion's proposal for slowly decaying
+  // spectra): the gathered sample Y in Ysum (rows kk..m, width bb) becomes
+  // (B B^T)^q Y on the rows kk..m of sx.  Each step is a reduce (Z = B^T Y as
+  // split partials), a formW with T = I / ||A||_F^2 (the scale keeps the
+  // products bounded and leaves the reflectors unchanged: QR of Y D has the
+  // reflectors of Y for positive diagonal D), a sample-only pass P = B Z and
+  // a gather back into Ysum.
+  auto power_steps = [&](int64_t kk, int64_t bb, const T* sx, int64_t ldsx, int64_t rows_pad,
+                         bool speculative) -> rrf_status {
+    const int64_t mpp = m - kk;
+    const int bpp = pad16(bb);
+    for (int it = 0; it < power; ++it) {
+      const int sr0 = red_splits(mpp, n, p->num_cus);
+      ReduceArgs<T> ra{};
+      ra.X = sx + kk; ra.ldx = ldsx; ra.mr = mpp; ra.n = n;
+      ra.V = p->Ysum; ra.ldv = p->sz.ldysum; ra.bp = bpp;
+      ra.Z = (T*)p->Zpart; ra.split_stride = n * bpp;
+      ra.rows_per_split = round_up(ceil_div(mpp, sr0), kRedChunk);
+      const int sr = (int)ceil_div(mpp, ra.rows_per_split);
+      const double fl = 2.0 * mpp * n * bb;
+      const double rby = e * mpp * n, wby = e * n * bb * (sr + 1);
+      RRF_LAUNCH(p, RRF_STAGE_SAMPLE, fl, rby, launch_reduce<T>(ra, sr, s));
+      FormWArgs<T> fa{};
+      fa.Z = (T*)p->Zpart; fa.nsplit = sr; fa.split_stride = ra.split_stride;
+      fa.Tm = p->Tpow; fa.ldt = 64; fa.W = (T*)p->W; fa.n = n; fa.bp = bpp;
+      fa.trans = 1; fa.b = (int)bb;
+      RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 1.0 * n * bb, wby, launch_formw<T>(fa, s));
+      UpdateArgs<T> us{};
+      us.src = sx + kk; us.lds = ldsx; us.dst = nullptr; us.ldd = 0; us.mr = mpp; us.n = n;
+      us.V = nullptr; us.ldv = 0; us.bp = 0; us.W = nullptr; us.ldw = 0;
+      us.Om = (T*)p->W; us.ldo = bpp; us.qp = bpp; us.P = Yp; us.ldp = ldb;
+      us.split_stride = ldb * 64; us.s0 = 0; us.normpart = nullptr;
+      us.cols_per_split = round_up(ceil_div(n, upd_splits(mpp, n, p->num_cus)), kUpdChunk);
+      const int sus = (int)ceil_div(n, us.cols_per_split);
+      const double uby = e * (mpp * n + mpp * bb);
+      RRF_LAUNCH(p, RRF_STAGE_SAMPLE, fl, uby, launch_update<T>(us, sus, s));
+      const double gby = e * mpp * bb * sus + 8.0 * mpp * bb;
+      RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 0.0, gby,
+                 launch_gather_panel<T>(Yp, ldb, ldb * 64, sus, mpp, (int)bb, bpp, rows_pad,
+                                        p->Ysum, p->sz.ldysum, s));
+      if (speculative)
+        spec(RRF_STAGE_SAMPLE, kk, 2.0 * fl + 1.0 * n * bb, rby + wby + uby + gby);
+    }
+    return RRF_OK;
+  };
+  // Spectral-norm estimate of B[kk:m, :] (spectral stop mode) from its
+  // sample Y = B[kk:m, :] Omega' (binary64, rows kk..m at Y, width bb, zero
+  // columns up to pad16(bb)): Z = B^T Y, the Gram matrices of Y and Z, and
+  // the largest eigenvalue of their pencil into the run state and trace.
+  auto spectral = [&](int64_t kk, int64_t bb, const double* Yy, int64_t ldyy,
+                      int trace_block) -> rrf_status {
+    const int64_t mpp = m - kk;
+    const int bpp = pad16(bb);
+    const int sr0 = red_splits(mpp, n, p->num_cus);
+    ReduceArgs<T> ra{};
+    ra.X = Bws + kk; ra.ldx = ldb; ra.mr = mpp; ra.n = n;
+    ra.V = Yy; ra.ldv = ldyy; ra.bp = bpp;
+    ra.Z = (T*)p->Zpart; ra.split_stride = n * bpp;
+    ra.rows_per_split = round_up(ceil_div(mpp, sr0), kRedChunk);
+    const int sr = (int)ceil_div(mpp, ra.rows_per_split);
+    RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 2.0 * mpp * n * bb, e * mpp * n,
+               launch_reduce<T>(ra, sr, s));
+    SpecGramArgs<T> ga{};
+    ga.Y = Yy; ga.ldy = ldyy; ga.my = mpp;
+    ga.Z = (T*)p->Zpart; ga.nsplit = sr; ga.split_stride = n * bpp; ga.nz = n;
+    ga.bp = bpp; ga.part = p->spec_part; ga.st = p->st;
+    RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 2.0 * (mpp + n) * bpp * bpp,
+               8.0 * mpp * bpp + e * n * bpp * sr, launch_spec_gram<T>(&ga, s));
+    SpecFinishArgs fa{};
+    fa.part = p->spec_part; fa.gy = ga.gy; fa.gz = ga.gz; fa.st = p->st;
+    fa.trace = p->trace_spec_d; fa.block = trace_block;
+    RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 8.0 * 4096 * (ga.gy + ga.gz),
+               launch_spec_finish(fa, s));
+    return RRF_OK;
   };
   while (!stop) {
     const int64_t bi = sub_width(k);
@@ -563,6 +650,11 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
         yoff = 0;
         s1_done = true;
       } else {
+        if (power > 0) {
+          rrf_status rs = power_steps(k, bi, sub == 0 ? A : Bws, sub == 0 ? lda : ldb,
+                                      sh.rows_pad, false);
+          if (rs != RRF_OK) return rs;
+        }
         RRF_LAUNCH(p, RRF_STAGE_PANEL, pflops, 16.0 * mp * bi,
                    run_panel(p, pa, route, sh, s));
       }
@@ -683,6 +775,21 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
                  launch_update<T>(ua, su, s));
     }
     if (b_s > 0) spec(RRF_STAGE_UPDATE, k_s, smp_flops, 0.0);
+    if (mode == RRF_STOP_SPECTRAL && at_end && b_next > 0) {
+      // The sample of the next sub-block (the next block's first columns)
+      // is B[k_next:m, :] Omega_next: with look-ahead it is already in Ysum
+      // (brought up to date for the panel inside the update's launch),
+      // otherwise the update's partials are gathered.
+      const double* Yy = p->Ysum + bi;
+      if (!la) {
+        RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, e * (mp - bi) * b_next * su,
+                   launch_gather_panel<T>(Yp + bi, ldb, ldb * 64, su, mp - bi, (int)b_next,
+                                          pad16(b_next), mp - bi, p->Yest, p->sz.ldysum, s));
+        Yy = p->Yest;
+      }
+      rrf_status rs = spectral(k_next, b_next, Yy, p->sz.ldysum, blk);
+      if (rs != RRF_OK) return rs;
+    }
     nparts = (int)(ceil_div(mp, kUpdRows) * su);
     RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
                launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
@@ -707,7 +814,8 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     // reads, stays above sigma^2 after this block; a wrong guess (the run
     // stops here after all) wastes that work, whose results lie past k and
     // are never used.
-    const double E_prev = mode ? p->st_host->E_sub : p->st_host->E_trail;
+    const double E_prev = mode == RRF_STOP_TRAILING ? p->st_host->E_trail
+                          : (mode == RRF_STOP_SUBTRACT ? p->st_host->E_sub : p->st_host->E_spec);
     const double E_pred =
         E_prev2 > 0.0 ? E_prev * std::min(1.0, E_prev / E_prev2) : E_prev;
     E_prev2 = E_prev;
@@ -747,6 +855,10 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       pn.V = V + k_next + k_next * ldb; pn.ldv = ldb;
       pn.Tm = Tm + k_next * kTLd; pn.ldt = kTLd; pn.tau = tau + k_next;
       pn.red = p->red; pn.rowj = p->rowj; pn.st = p->st; pn.G = shn.G;
+      if (power > 0) {
+        rrf_status rs = power_steps(k_next, b_next, Bws, ldb, shn.rows_pad, true);
+        if (rs != RRF_OK) return rs;
+      }
       const double pfl = panel_flops((double)mpn, (double)b_next), pby = 16.0 * mpn * b_next;
       RRF_LAUNCH(p, RRF_STAGE_PANEL, pfl, pby, run_panel(p, pn, route_n, shn, s));
       spec(RRF_STAGE_PANEL, k_next, pfl, pby + gby);
@@ -820,16 +932,25 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   if (blk > 0) {
     p->trace_trail.resize(blk);
     p->trace_sub.resize(blk);
+    p->trace_spec.assign(blk, std::nan(""));
     he = hipMemcpy(p->trace_trail.data(), p->trace_trail_d, blk * sizeof(double),
                    hipMemcpyDeviceToHost);
     if (he == hipSuccess)
       he = hipMemcpy(p->trace_sub.data(), p->trace_sub_d, blk * sizeof(double),
                      hipMemcpyDeviceToHost);
+    // The estimate exists for the blocks that ended below the cap, and only
+    // in spectral mode.
+    const int nspec = mode == RRF_STOP_SPECTRAL ? (k < kcap ? blk : blk - 1) : 0;
+    if (he == hipSuccess && nspec > 0)
+      he = hipMemcpy(p->trace_spec.data(), p->trace_spec_d, nspec * sizeof(double),
+                     hipMemcpyDeviceToHost);
     if (he != hipSuccess) return hip_fail(he);
   }
   p->E0 = p->st_host->E0;
   p->sigma2 = p->st_host->sigma2;
-  const double E = mode ? p->st_host->E_sub : p->st_host->E_trail;
+  // Spectral mode: at the cap there is no estimate; the Frobenius norm (an
+  // upper bound of the spectral norm) decides the warning.
+  const double E = mode == RRF_STOP_SUBTRACT ? p->st_host->E_sub : p->st_host->E_trail;
   *warn_kmax = k == kcap && kcap < std::min(m, n) && E > p->sigma2;
   *k_out = k;
   return RRF_OK;
@@ -962,6 +1083,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   p->k_max = k_max;
   p->stream = (hipStream_t)hip_stream;
   p->stop_mode = RRF_STOP_TRAILING;
+  p->power = 0;
   p->timing = 0;
   p->panel_target = 64;
   p->panel_launches = 0;
@@ -1035,8 +1157,12 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   RRF_ALLOC(gx, p->sz.gx);
   RRF_ALLOC(tx, p->sz.tx);
   RRF_ALLOC(st, p->sz.st);
-  RRF_ALLOC(trace_trail_d, p->sz.trace / 2);
-  RRF_ALLOC(trace_sub_d, p->sz.trace / 2);
+  RRF_ALLOC(trace_trail_d, p->sz.trace / 3);
+  RRF_ALLOC(trace_sub_d, p->sz.trace / 3);
+  RRF_ALLOC(trace_spec_d, p->sz.trace / 3);
+  RRF_ALLOC(Yest, p->sz.Yest);
+  RRF_ALLOC(spec_part, p->sz.spec);
+  RRF_ALLOC(Tpow, p->sz.Tpow);
 #undef RRF_ALLOC
   if (e == hipSuccess) {
     ++counter;
@@ -1056,6 +1182,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   }
   if (e == hipSuccess) e = hipMemsetAsync(p->Om, 0, p->sz.Om, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->V, 0, p->sz.V, p->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(p->Yest, 0, p->sz.Yest, p->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(p->stream);
   if (e != hipSuccess) {
     free_plan(p);
@@ -1077,9 +1204,16 @@ rrf_status rrf_destroy(rrf_plan_t plan) {
 }
 
 rrf_status rrf_set_stop_mode(rrf_plan_t plan, rrf_stop_mode mode) {
-  if (!plan || (mode != RRF_STOP_TRAILING && mode != RRF_STOP_SUBTRACT))
+  if (!plan || (mode != RRF_STOP_TRAILING && mode != RRF_STOP_SUBTRACT &&
+                mode != RRF_STOP_SPECTRAL))
     return RRF_ERR_INVALID_ARG;
   plan->stop_mode = mode;
+  return RRF_OK;
+}
+
+rrf_status rrf_set_power_iterations(rrf_plan_t plan, int q) {
+  if (!plan || q < 0 || q > kMaxPower) return RRF_ERR_INVALID_ARG;
+  plan->power = q;
   return RRF_OK;
 }
 
@@ -1096,6 +1230,10 @@ rrf_status rrf_run(rrf_plan_t plan, const void* A, int64_t m, int64_t n,
   if (m < 0 || n < 0 || lda < std::max<int64_t>(1, m)) return RRF_ERR_INVALID_ARG;
   if (!std::isfinite(tol) || tol < 0.0) return RRF_ERR_INVALID_ARG;
   if (block_b < 1 || block_b > plan->b_max) return RRF_ERR_INVALID_ARG;
+  // Power iterations act on a whole block's sample at once; blocks wider
+  // than one 64-column sub-block would power their second part on the
+  // deflated matrix instead.
+  if (plan->power > 0 && block_b > kMaxBlock) return RRF_ERR_INVALID_ARG;
   if (m > plan->m_max || n > plan->n_max) return RRF_ERR_SHAPE;
   stats_reset(plan);
   plan->last_m = m;
@@ -1131,7 +1269,7 @@ rrf_status rrf_run(rrf_plan_t plan, const void* A, int64_t m, int64_t n,
 }
 
 rrf_status rrf_get_trace(rrf_plan_t plan, int64_t cap, int64_t* nblocks,
-                         double* E_trail, double* E_sub, double* E0,
+                         double* E_trail, double* E_sub, double* E_spec, double* E0,
                          double* sigma2) {
   if (!plan || !nblocks || cap < 0 || (cap > 0 && (!E_trail || !E_sub)))
     return RRF_ERR_INVALID_ARG;
@@ -1140,6 +1278,7 @@ rrf_status rrf_get_trace(rrf_plan_t plan, int64_t cap, int64_t* nblocks,
   for (int64_t i = 0; i < nw; ++i) {
     E_trail[i] = plan->trace_trail[i];
     E_sub[i] = plan->trace_sub[i];
+    if (E_spec) E_spec[i] = plan->trace_spec[i];
   }
   if (E0) *E0 = plan->E0;
   if (sigma2) *sigma2 = plan->sigma2;

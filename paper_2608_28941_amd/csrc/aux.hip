@@ -9,7 +9,8 @@ namespace {
 // Sums the per-workgroup norm partials in a fixed order (deterministic) and
 // applies the stop test.  init: E0 = ||A||_F^2, sigma^2 = tol^2 E0.
 // Otherwise: E_trail = ||B[k:m, :]||^2 directly, E_sub -= ||B_i||^2 (the
-// paper's running difference, clamped at 0).  At the end of a block (block
+// paper's running difference, clamped at 0); in spectral mode (2) the
+// estimate the spectral kernels left in the run state.  At the end of a block (block
 // >= 0: the trace index) the stop test runs: stop iff E <= sigma^2 or the
 // rank cap is reached (Sec. 4: the loop ends after at most min(m, n) / b
 // blocks); inside a block (block < 0, the first 64 columns of a wider
@@ -43,6 +44,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     st->sigma2 = (tol * tol) * E0;
     st->E_trail = E0;
     st->E_sub = E0;
+    st->E_spec = E0;
     st->stop = st->nonfinite || !(E0 > st->sigma2) || k_cap == 0;
     st->barrier_err = 0;
   } else {
@@ -54,7 +56,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     if (block >= 0) {
       tt[block] = trail;
       ts[block] = es;
-      const double E = mode ? es : trail;
+      const double E = mode == 0 ? trail : (mode == 1 ? es : st->E_spec);
       st->stop = st->nonfinite || st->barrier_err || !(E > st->sigma2) ||
                  k_after >= k_cap;
     } else {

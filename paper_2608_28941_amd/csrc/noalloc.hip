@@ -48,7 +48,7 @@ __global__ void na_clear_kernel(unsigned long long* words, int64_t nwords, DevSt
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < nwords) words[i] = 0ull;
   if (i == 0) {
-    st->E0 = st->sigma2 = st->E_trail = st->E_sub = 0.0;
+    st->E0 = st->sigma2 = st->E_trail = st->E_sub = st->E_spec = 0.0;
     st->stop = st->nonfinite = st->barrier_err = 0;
     st->spin_limit = spin_limit;
   }

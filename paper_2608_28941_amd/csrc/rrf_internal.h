@@ -12,6 +12,7 @@ namespace rrf {
 // Tiling constants (see each kernel for its use).
 constexpr int kMaxBlock = 64;      // widest sub-block / panel (MFMA tiles of 16)
 constexpr int kMaxBlockB = 128;    // largest block size b of a run (sub-blocks of <= 64)
+constexpr int kMaxPower = 8;       // largest number of power iterations per sample
 constexpr int kUpdRowTiles = 2;    // 16-row tiles per update wavefront
 constexpr int kUpdRows = 128;      // rows per update workgroup (4 waves x 2 x 16)
 constexpr int kUpdChunk = 16;      // columns per staged chunk in the update
@@ -40,6 +41,7 @@ struct DevState {
   int barrier_err;  // 1: a grid-wide wait gave up (sticky until cleared)
   unsigned spin_limit;  // poll rounds before a grid-wide wait gives up; 0:
                         // every wait gives up at its first poll (tests)
+  double E_spec;    // spectral-norm estimate of ||B[k:m, :]||_2^2 (spectral mode)
 };
 
 // Launch descriptors -------------------------------------------------------
@@ -228,6 +230,32 @@ hipError_t launch_gather_panel(const T* P, int64_t ldp, int64_t split_stride,
                                int nsplit, int64_t m, int b, int bp,
                                int64_t rows_pad, double* Ysum, int64_t ldy,
                                hipStream_t s);
+
+// Spectral-norm estimate (spectral.hip).  Y: my x bp binary64 (ldy, zero
+// columns up to bp); Z: split partials Z_s[row * bp + c] of nz rows (T).
+// The launcher sets gy, gz (workgroups per matrix) and the row ranges; part
+// holds (gy + gz) x 64 x 64 doubles.
+constexpr int kMaxSpecWGs = 128;
+template <typename T>
+struct SpecGramArgs {
+  const double* Y; int64_t ldy; int64_t my;
+  const T* Z; int nsplit; int64_t split_stride; int64_t nz;
+  int bp;
+  double* part;
+  const DevState* st;          // E0 scales the values
+  int gy, gz;
+  int64_t rows_per_wg_y, rows_per_wg_z;
+};
+struct SpecFinishArgs {
+  const double* part; int gy, gz;
+  DevState* st;
+  double* trace; int block;    // trace[block] = estimate (block >= 0)
+};
+template <typename T>
+hipError_t launch_spec_gram(SpecGramArgs<T>* a, hipStream_t s);
+hipError_t launch_spec_finish(const SpecFinishArgs& a, hipStream_t s);
+// Tm (64 x 64, ldt) = I / ||A||_F^2, the W factor of a power step.
+hipError_t launch_scaled_identity(double* Tm, int64_t ldt, const DevState* st, hipStream_t s);
 
 hipError_t launch_finalize(const double* normpart, int nparts, DevState* st,
                            double* trace_trail, double* trace_sub, int block,

@@ -73,7 +73,8 @@ def test_invalid_arguments_rejected_before_device():
     assert lib.rrf_set_timing(None, 1) == E
     assert lib.rrf_set_stop_mode(None, 0) == E
     nb = ctypes.c_int64()
-    assert lib.rrf_get_trace(None, 0, ctypes.byref(nb), None, None, None, None) == E
+    assert lib.rrf_get_trace(None, 0, ctypes.byref(nb), None, None, None, None, None) == E
+    assert lib.rrf_set_power_iterations(None, 1) == E
     assert lib.rrf_sketch(1, 0, -1, 0, 1, ctypes.c_void_p(8), 1, None) == E
     assert lib.rrf_sketch(1, 0, 10, 0, 1, None, 10, None) == E
     assert lib.rrf_sketch(1, 0, 10, 0, 1, ctypes.c_void_p(8), 5, None) == E
