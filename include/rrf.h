@@ -237,16 +237,19 @@ rrf_status rrf_apply_block_reflector(rrf_plan_t plan, int trans,
 /* GaLore subspace-consistency map (Sec. 7): a low-rank state M_t expressed
  * in the basis Q_t, carried to the next basis Q_{t+1}:
  *   out = Qnew^T (Qold M)      (r_new x n),
- * formed as C = Qnew^T Qold (r_new x r_old) and then C M: two dense GEMMs
- * (rocBLAS, the plan's dtype) on the plan's stream, asynchronous.
+ * formed as C = Qnew^T Qold (r_new x r_old, the m-row reduction split over
+ * workgroups and summed in a fixed order) and then C M, by the library's own
+ * MFMA kernels in the plan's dtype on the plan's stream, asynchronous.
  * Qnew: m x r_new (ldqn), Qold: m x r_old (ldqo), M: r_old x n (ldm),
  * out: r_new x n (ldo), device pointers, column-major; out must not alias
  * the inputs.  Either basis may come from rrf_run or anywhere else (no
- * orthonormality is assumed).  C lives in plan-owned device memory that
- * grows on demand (a call may allocate).  r_old = 0 or m = 0 gives out = 0.
+ * orthonormality is assumed).  C and its split partials live in plan-owned
+ * device memory that grows on demand (a call may allocate).  r_old = 0 or
+ * m = 0 gives out = 0.
  * Errors: RRF_ERR_INVALID_ARG for a null pointer to a nonempty matrix,
- * negative sizes or short leading dimensions; RRF_ERR_SHAPE for a size beyond 2^31 - 1;
- * RRF_ERR_NOMEM, RRF_ERR_HIP on allocation or library failure. */
+ * negative sizes or short leading dimensions; RRF_ERR_SHAPE for a size beyond
+ * 2^31 - 1 or n, r_old beyond 65535 x 64; RRF_ERR_NOMEM, RRF_ERR_HIP on
+ * allocation or launch failure. */
 rrf_status rrf_subspace_map(rrf_plan_t plan, const void* Qnew, int64_t ldqn,
                             int64_t r_new, const void* Qold, int64_t ldqo,
                             int64_t r_old, const void* M, int64_t ldm,

@@ -4,8 +4,8 @@
 
 Every source is compiled with hipcc for gfx950 with packed FP32 instructions
 disabled; the sketch generator is also compiled without FP contraction (its
-results must be bit-reproducible from the definition).  The library links
-rocBLAS for the two dense GEMMs of the subspace map.
+results must be bit-reproducible from the definition).  No vendor math
+library is linked: every kernel is in csrc/.
 """
 
 import concurrent.futures as cf
@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librrf.so")
 
-SOURCES = ["sketch.hip", "panel.hip", "panel_gram.hip", "tsqr.hip", "thin_apply.hip", "wy.hip", "lookahead.hip", "aux.hip", "spectral.hip", "noalloc.hip", "abi.cpp"]
+SOURCES = ["sketch.hip", "panel.hip", "panel_gram.hip", "tsqr.hip", "thin_apply.hip", "wy.hip", "lookahead.hip", "aux.hip", "spectral.hip", "map.hip", "noalloc.hip", "abi.cpp"]
 COMMON = [
     "-x", "hip", "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",
     "-Wall", "-Wno-unused-function",
@@ -56,8 +56,7 @@ def build(verbose=False, jobs=None):
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(lambda s: _compile(hipcc, s, verbose), SOURCES))
     tmp = LIB + ".tmp"
-    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs,
-           "-L/opt/rocm/lib", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib", "-o", tmp]
+    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

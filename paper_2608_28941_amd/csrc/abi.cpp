@@ -16,7 +16,6 @@
 // block applications costs about 2 sqrt(s) u sqrt(k) in ||Q^T Q - I||_F.
 
 #include <hip/hip_runtime.h>
-#include <rocblas/rocblas.h>
 
 #include <algorithm>
 #include <cmath>
@@ -139,8 +138,7 @@ struct rrf_plan {
   int64_t launches[RRF_NUM_STAGES];
   std::vector<hipEvent_t> events;
   hipEvent_t state_ev = nullptr;   // the run state's copy to the host has landed
-  rocblas_handle blas = nullptr;   // subspace map (created on first use)
-  void* map_c = nullptr;           // its r_new x r_old product
+  void* map_c = nullptr;           // subspace map: split partials and C
   size_t map_c_bytes = 0;
   std::vector<int> event_stage;
   size_t events_used;
@@ -170,7 +168,6 @@ void free_plan(rrf_plan* p) {
   if (p->st_host) (void)hipHostFree(p->st_host);
   for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
   if (p->state_ev) (void)hipEventDestroy(p->state_ev);
-  if (p->blas) (void)rocblas_destroy_handle(p->blas);
   if (p->map_c) (void)hipFree(p->map_c);
   delete p;
 }
@@ -1400,14 +1397,10 @@ rrf_status rrf_subspace_map(rrf_plan_t plan, const void* Qnew, int64_t ldqn,
     hipError_t he = hipMemset2DAsync(out, (size_t)ldo * e, 0, (size_t)r_new * e, (size_t)n, s);
     return he == hipSuccess ? RRF_OK : hip_fail(he);
   }
-  if (!plan->blas) {
-    if (rocblas_create_handle(&plan->blas) != rocblas_status_success) {
-      plan->blas = nullptr;
-      return RRF_ERR_HIP;
-    }
-  }
-  if (rocblas_set_stream(plan->blas, s) != rocblas_status_success) return RRF_ERR_HIP;
-  const size_t need = (size_t)r_new * (size_t)r_old * e;
+  // Grid limits of the tiled kernels (64 x 64 output tiles).
+  if (ceil_div(n, 64) > 65535 || ceil_div(r_old, 64) > 65535) return RRF_ERR_SHAPE;
+  const int nsplit = map_splits(r_new, r_old, m, plan->num_cus);
+  const size_t need = (size_t)(nsplit + 1) * (size_t)r_new * (size_t)r_old * e;
   if (need > plan->map_c_bytes) {
     if (plan->map_c) {
       (void)hipFree(plan->map_c);
@@ -1420,31 +1413,19 @@ rrf_status rrf_subspace_map(rrf_plan_t plan, const void* Qnew, int64_t ldqn,
     }
     plan->map_c_bytes = need;
   }
-  const rocblas_int mi = (rocblas_int)m, ni = (rocblas_int)n;
-  const rocblas_int r1 = (rocblas_int)r_new, r0 = (rocblas_int)r_old;
-  rocblas_status bs;
+  hipError_t he;
   if (plan->dtype == RRF_F64) {
-    const double one = 1.0, zero = 0.0;
-    double* C = (double*)plan->map_c;
-    bs = rocblas_dgemm(plan->blas, rocblas_operation_transpose, rocblas_operation_none,
-                       r1, r0, mi, &one, (const double*)Qnew, (rocblas_int)ldqn,
-                       (const double*)Qold, (rocblas_int)ldqo, &zero, C, r1);
-    if (bs == rocblas_status_success)
-      bs = rocblas_dgemm(plan->blas, rocblas_operation_none, rocblas_operation_none,
-                         r1, ni, r0, &one, C, r1, (const double*)M, (rocblas_int)ldm,
-                         &zero, (double*)out, (rocblas_int)ldo);
+    double* Cp = (double*)plan->map_c;
+    he = launch_subspace_map<double>((const double*)Qnew, ldqn, r_new, (const double*)Qold,
+                                     ldqo, r_old, (const double*)M, ldm, m, n, (double*)out,
+                                     ldo, Cp, Cp + (size_t)nsplit * r_new * r_old, nsplit, s);
   } else {
-    const float one = 1.0f, zero = 0.0f;
-    float* C = (float*)plan->map_c;
-    bs = rocblas_sgemm(plan->blas, rocblas_operation_transpose, rocblas_operation_none,
-                       r1, r0, mi, &one, (const float*)Qnew, (rocblas_int)ldqn,
-                       (const float*)Qold, (rocblas_int)ldqo, &zero, C, r1);
-    if (bs == rocblas_status_success)
-      bs = rocblas_sgemm(plan->blas, rocblas_operation_none, rocblas_operation_none,
-                         r1, ni, r0, &one, C, r1, (const float*)M, (rocblas_int)ldm,
-                         &zero, (float*)out, (rocblas_int)ldo);
+    float* Cp = (float*)plan->map_c;
+    he = launch_subspace_map<float>((const float*)Qnew, ldqn, r_new, (const float*)Qold, ldqo,
+                                    r_old, (const float*)M, ldm, m, n, (float*)out, ldo, Cp,
+                                    Cp + (size_t)nsplit * r_new * r_old, nsplit, s);
   }
-  return bs == rocblas_status_success ? RRF_OK : RRF_ERR_HIP;
+  return he == hipSuccess ? RRF_OK : hip_fail(he);
 }
 
 rrf_status rrf_copy_matrix(rrf_dtype dtype, const void* src, int64_t lds,

@@ -257,6 +257,16 @@ hipError_t launch_spec_finish(const SpecFinishArgs& a, hipStream_t s);
 // Tm (64 x 64, ldt) = I / ||A||_F^2, the W factor of a power step.
 hipError_t launch_scaled_identity(double* Tm, int64_t ldt, const DevState* st, hipStream_t s);
 
+// GaLore subspace map (map.hip): out = (Q_new^T Q_old) M with split-K
+// partials Cpart (nsplit x r_new x r_old) and C (r_new x r_old).
+constexpr int kMaxMapSplits = 16;
+int map_splits(int64_t r_new, int64_t r_old, int64_t m, int num_cus);
+template <typename T>
+hipError_t launch_subspace_map(const T* Qnew, int64_t ldqn, int64_t r_new, const T* Qold,
+                               int64_t ldqo, int64_t r_old, const T* M, int64_t ldm,
+                               int64_t m, int64_t n, T* out, int64_t ldo, T* Cpart,
+                               T* C, int nsplit, hipStream_t s);
+
 hipError_t launch_finalize(const double* normpart, int nparts, DevState* st,
                            double* trace_trail, double* trace_sub, int block,
                            int64_t k_after, int64_t k_cap, int mode,
