@@ -2,10 +2,12 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline]
-    python bench.py --fixed-rank R[,R..]  fixed-rank mode (k_max = R, tol = 0)
-                                          against a one-shot pipeline with the
-                                          same sketch (rocBLAS GEMMs, rocSOLVER
-                                          QR through torch), Sec. 6 / Fig. 6
+    python bench.py --fixed-rank R[,R..] [--fixed-block B]
+                                          fixed-rank mode (k_max = R, tol = 0,
+                                          b = 128) against one-shot pipelines
+                                          with the same sketch: QR and orgqr
+                                          on this library's kernels, and
+                                          rocSOLVER (Sec. 6 / Fig. 6)
     python bench.py --copy-probe MIB      one plain device copy of MIB MiB
                                           (calibrates the HBM byte counters)
     python bench.py --summarize DIR...    per-kernel summary of rocprofv3 CSVs
@@ -53,6 +55,8 @@ def parse():
                     help="extra runs with per-kernel HIP-event timing")
     ap.add_argument("--fixed-rank", default=None, metavar="R[,R..]",
                     help="only the fixed-rank comparison at these ranks")
+    ap.add_argument("--fixed-block", type=int, default=128,
+                    help="block size b of the fixed-rank runs (Fig. 6: 128)")
     ap.add_argument("--subspace-map", action="store_true",
                     help="only time the GaLore subspace map (Sec. 7) on galore-sized bases")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -244,13 +248,43 @@ def summarize(dirs):
     print("\n".join(lines))
 
 
+def oneshot_lib(plan, A, Om, pb=64):
+    """One-shot fixed-rank range finder on this library's kernels: Y = A Omega
+    (one vendor GEMM), blocked Householder QR of Y with the library's panel QR
+    (rrf_panel_qr) and block reflector (rrf_apply_block_reflector) in
+    pb-column panels, Q = H_0 .. H_{r-1} [I_r; 0] backward with the same
+    block reflector (orgqr), and B = Q^T A (one vendor GEMM).  A and Omega
+    column-major; returns (Q, B) column-major / row-major."""
+    import torch
+    m = A.shape[0]
+    r = Om.shape[1]
+    Y = (Om.t() @ A.t()).t()                 # m x r, column-major
+    refl = []
+    for j in range(0, r, pb):
+        jb = min(pb, r - j)
+        V, T, _ = plan.panel_qr(Y[j:, j:j + jb])
+        if j + jb < r:
+            plan.apply_block_reflector(V, T, Y[j:, j + jb:], trans=True)
+        refl.append((j, V, T))
+    Q = torch.zeros(r, m, dtype=A.dtype, device=A.device).t()
+    Q[:r, :r] = torch.eye(r, dtype=A.dtype, device=A.device)
+    for j, V, T in reversed(refl):
+        plan.apply_block_reflector(V, T, Q[j:, j:], trans=False)
+    B = Q.t() @ A
+    return Q, B
+
+
 def fixed_rank(a):
     """Fixed-rank mode (Sec. 6, Fig. 6): rrf_run with k_max = r and tol = 0
-    (r columns in r / b blocks, RRF_WARN_KMAX expected) against the one-shot
-    fixed-rank range finder on the same GPU and the same sketch Omega
-    (columns 0..r-1 of RRF-NORMAL-v1): Y = A Omega, Q = qr(Y) (rocSOLVER
-    geqrf + orgqr via torch), B = Q^T A.  The reference pipeline is a
-    measurement only.  Prints one JSON line."""
+    (r columns in r / b blocks, RRF_WARN_KMAX expected) at b = a.fixed_block
+    against two one-shot fixed-rank range finders on the same GPU and the
+    same sketch Omega (columns 0..r-1 of RRF-NORMAL-v1):
+      lib:       Y = A Omega, blocked QR and orgqr on this library's panel
+                 and block-reflector kernels, B = Q^T A (oneshot_lib);
+      rocsolver: Y = A Omega, Q from torch.linalg.qr (rocSOLVER geqrf +
+                 orgqr), B = Q^T A.
+    Both comparators use the vendor GEMM for the two products.  Prints one
+    JSON line."""
     import torch
     import paper_2608_28941_amd as rrf
     import workloads as W
@@ -260,9 +294,10 @@ def fixed_rank(a):
     torch.cuda.set_device(dev)
     tdt = torch.float64 if w.dtype == "float64" else torch.float32
     A = rrf.colmajor(torch.from_numpy(A_host).to(dev))
-    Ar = A.contiguous()                       # row-major copy for torch's GEMMs
+    del A_host
     normA = float(torch.linalg.norm(A.double()))
     ranks = [int(x) for x in a.fixed_rank.split(",")]
+    b = a.fixed_block
     out = []
 
     def timed(fn, reps):
@@ -270,41 +305,57 @@ def fixed_rank(a):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(reps):
-            r = fn()
+            res = fn()
         torch.cuda.synchronize()
-        return (time.perf_counter() - t0) / reps, r
+        return (time.perf_counter() - t0) / reps, res
 
-    for r in ranks:
-        b = min(w.block_b, 64)
-        with rrf.Plan(tdt, w.m, w.n, b, k_max=r) as plan:
-            def ours():
-                return plan.run_raw(A, 0.0, b, w.sketch_seed)
-            t_ours, res = timed(ours, a.steps)
-            k = res[2]
-            Q, B, _ = plan.run(A, 0.0, b, w.sketch_seed)
-            res_ours = float(torch.linalg.norm((A - Q @ B).double())) / normA
-        Om = rrf.sketch(tdt, w.sketch_seed, w.n, 0, r)
+    def rel_res(Q, B):
+        num = 0.0
+        for c0 in range(0, A.shape[1], 2048):
+            R = A[:, c0:c0 + 2048] - Q @ B[:, c0:c0 + 2048]
+            num += float((R.double() ** 2).sum())
+        return num ** 0.5 / normA
 
-        def oneshot():
-            Y = Ar @ Om
-            Qo, _ = torch.linalg.qr(Y)
-            Bo = Qo.t().contiguous() @ Ar
-            return Qo, Bo
-        t_ref, (Qo, Bo) = timed(oneshot, a.steps)
-        res_ref = float(torch.linalg.norm((Ar - Qo @ Bo).double())) / normA
-        fl = algorithmic_flops(w.m, w.n, k, b)
-        fl_ref = 2.0 * w.m * w.n * r + 4.0 * w.m * r * r - 4.0 / 3.0 * r ** 3 + 2.0 * w.m * w.n * r
-        out.append({"r": r, "k": k, "ours_ms": round(t_ours * 1e3, 3),
-                    "ours_gflops": round(fl / t_ours / 1e9, 1),
-                    "ours_residual": res_ours,
-                    "oneshot_ms": round(t_ref * 1e3, 3),
-                    "oneshot_gflops": round(fl_ref / t_ref / 1e9, 1),
-                    "oneshot_residual": res_ref})
-        print(f"[fixed-rank] r={r} ours {t_ours*1e3:.2f} ms one-shot {t_ref*1e3:.2f} ms",
-              file=sys.stderr, flush=True)
-        del Om, Qo, Bo
-    print(json.dumps({"metric": "fixed-rank wall time (ms), ours vs one-shot pipeline",
-                      "workload": w.name, "dtype": w.dtype, "block_b": min(w.block_b, 64),
+    with rrf.Plan(tdt, w.m, w.n, 64) as lib_plan:
+        for r in ranks:
+            print(f"[fixed-rank] r={r} b={b}", file=sys.stderr, flush=True)
+            with rrf.Plan(tdt, w.m, w.n, b, k_max=r) as plan:
+                t_ours, res = timed(lambda: plan.run_raw(A, 0.0, b, w.sketch_seed), a.steps)
+                k = res[2]
+                Q, B, _ = plan.run(A, 0.0, b, w.sketch_seed)
+                res_ours = rel_res(Q, B)
+                del Q, B
+            Om = rrf.sketch(tdt, w.sketch_seed, w.n, 0, r)
+            t_lib, (Ql, Bl) = timed(lambda: oneshot_lib(lib_plan, A, Om), a.steps)
+            res_lib = rel_res(Ql, Bl)
+            orth_lib = float(torch.linalg.norm(Ql.t() @ Ql - torch.eye(r, dtype=tdt, device=dev)))
+            del Ql, Bl
+            Ar = A.contiguous()
+
+            def roc():
+                Qo, _ = torch.linalg.qr(Ar @ Om)
+                return Qo, Qo.t().contiguous() @ Ar
+            t_roc, (Qo, Bo) = timed(roc, a.steps)
+            del Ar
+            res_roc = rel_res(Qo, Bo)
+            del Qo, Bo, Om
+            fl = algorithmic_flops(w.m, w.n, k, b)
+            fl_one = (4.0 * w.m * w.n * r + 4.0 * w.m * r * r - 4.0 / 3.0 * r ** 3)
+            out.append({"r": r, "k": k, "ours_ms": round(t_ours * 1e3, 3),
+                        "ours_gflops": round(fl / t_ours / 1e9, 1),
+                        "ours_residual": res_ours,
+                        "oneshot_lib_ms": round(t_lib * 1e3, 3),
+                        "oneshot_lib_gflops": round(fl_one / t_lib / 1e9, 1),
+                        "oneshot_lib_residual": res_lib, "oneshot_lib_orth": orth_lib,
+                        "rocsolver_ms": round(t_roc * 1e3, 3),
+                        "rocsolver_gflops": round(fl_one / t_roc / 1e9, 1),
+                        "rocsolver_residual": res_roc})
+            print(f"[fixed-rank] r={r} ours {t_ours*1e3:.2f} ms, one-shot (library kernels) "
+                  f"{t_lib*1e3:.2f} ms, one-shot (rocSOLVER) {t_roc*1e3:.2f} ms",
+                  file=sys.stderr, flush=True)
+    print(json.dumps({"metric": "fixed-rank wall time (ms): adaptive range finder with "
+                                "k_max = r vs one-shot pipelines",
+                      "workload": w.name, "dtype": w.dtype, "block_b": b,
                       "steps": a.steps, "results": out}))
 
 
@@ -380,18 +431,28 @@ def algorithmic_flops(m, n, k, b):
     return f
 
 
-def cpu_baseline(A_host, w, budget_cols=1024, kmax=None):
-    """The oracle (numpy, float64) on a bounded sample: the first block of
-    Alg. 2 on the first ``budget_cols`` columns of the same matrix."""
-    import numpy as np
-    from oracle import hbarrf
+def blas_info():
+    """The BLAS library numpy runs on (threadpoolctl): vendor, version, threads."""
     try:
         import threadpoolctl
-        info = threadpoolctl.threadpool_info()
-        cores = max((d.get("num_threads", 1) for d in info
-                     if d.get("user_api") == "blas"), default=1)
+        for d in threadpoolctl.threadpool_info():
+            if d.get("user_api") == "blas":
+                return {"internal_api": d.get("internal_api"), "version": d.get("version"),
+                        "num_threads": int(d.get("num_threads", 1))}
     except Exception:
-        cores = os.cpu_count() or 1
+        pass
+    return {"internal_api": None, "version": None, "num_threads": os.cpu_count() or 1}
+
+
+def cpu_baseline(A_host, w, budget_cols=1024, kmax=None):
+    """The oracle (numpy, float64) on a bounded sample: the first block of
+    Alg. 2 on the first ``budget_cols`` columns of the same matrix; next to
+    it the whole oracle (Alg. 2 to the tolerance, explicit Q) on the
+    500 x 300 fp64 workload, one warm-up and the mean of three runs."""
+    import numpy as np
+    import workloads as W
+    from oracle import hbarrf
+    blas = blas_info()
     nc = min(budget_cols, A_host.shape[1])
     As = np.asfortranarray(A_host[:, :nc])
     kmax = kmax or w.block_b
@@ -399,11 +460,21 @@ def cpu_baseline(A_host, w, budget_cols=1024, kmax=None):
     r = hbarrf(As, 0.0, w.block_b, w.sketch_seed, k_max=kmax, dtype=w.np_dtype)
     dt = time.perf_counter() - t0
     fl = algorithmic_flops(As.shape[0], nc, r.k, w.block_b)
-    return {"value": fl / dt / 1e9, "unit": "GFLOP/s", "cores": int(cores),
-            "kind": "oracle", "seconds": dt,
+    wt = W.WORKLOADS["tiny_fp64_500x300"]
+    At = W.build_matrix(wt)
+    hbarrf(At, wt.tol, wt.block_b, wt.sketch_seed)
+    t1 = time.perf_counter()
+    for _ in range(3):
+        rt = hbarrf(At, wt.tol, wt.block_b, wt.sketch_seed)
+    dtt = (time.perf_counter() - t1) / 3
+    flt = algorithmic_flops(wt.m, wt.n, rt.k, wt.block_b)
+    return {"value": fl / dt / 1e9, "unit": "GFLOP/s", "cores": blas["num_threads"],
+            "kind": "oracle", "seconds": dt, "blas": blas,
             "sample": (f"first block (k={r.k}) of Alg. 2 on A[:, :{nc}] of "
                        f"{w.name} ({As.shape[0]}x{nc}), numpy float64, "
-                       f"one reflector at a time")}
+                       f"one reflector at a time"),
+            "whole_run_tiny": {"workload": wt.name, "k": rt.k, "ms": dtt * 1e3,
+                               "gflops": flt / dtt / 1e9}}
 
 
 def main():
