@@ -126,6 +126,8 @@ struct rrf_plan {
   DevState* st;
   DevState* st_host;
   int stop_mode, timing, panel_target;
+  int gram_fused_max;         // most workgroups of a Gram panel inside the update's launch
+  int sub_max;                // widest sub-block (16, 32 or 64 columns; 0: by size)
   unsigned spin_limit;       // poll rounds of a grid-wide wait (run state)
   unsigned panel_launches;   // epochs of the panel's tagged partials
   // last run
@@ -286,8 +288,8 @@ hipError_t read_state(rrf_plan* p) {
 
 // The panel algorithm for a block of b columns.  Narrow panels take the Gram
 // form (its column steps are cheap at 32 columns and it exchanges once per
-// sweep); 64-column panels take the column-by-column grid, which the
-// look-ahead hides inside the update.
+// sweep); 64-column panels take the column-by-column grid.  The look-ahead
+// hides either inside the update.
 int panel_alg(const rrf_plan* p, int64_t b) {
   if (p->panel_mode != kPanelAuto) return p->panel_mode;
   return pad16(b) <= 32 ? kPanelGram : kPanelGrid;
@@ -419,10 +421,28 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   // block's first 64 columns, updating, and sampling the rest from the
   // updated B gives the block's reflectors (Q_1^T (B Omega_2) =
   // (Q_1^T B) Omega_2).  The stop test runs at the end of each block only.
+  //
+  // The sub-block width: 64 columns, or 32 when the matrix is small (at most
+  // 512 MiB).  There a 64-column update is short beside the 64-column panel
+  // factored inside its launch (4096 x 11008 fp32: about 100 us against
+  // 300 us), while 32-column sub-blocks put a Gram panel of about the
+  // update's length beside each update (15.1 -> 12.7 ms per run there; at
+  // 16384 x 16384 fp64 64 columns stay faster, 33.5 against 45.6 ms).
+  // The spectral stop test estimates from the next block's first min(b, 64)
+  // sketch columns, the sample of a 64-column sub-block.
+  int sub_max = mode == RRF_STOP_SPECTRAL ? kMaxBlock : p->sub_max;
+  if (sub_max == 0) {
+    sub_max = kMaxBlock;
+    PanelShape sh32;
+    if (p->lookahead != 0 && p->power == 0 && p->panel_mode == kPanelAuto &&
+        std::min(b, kcap) > 32 && (double)m * (double)n * e <= 512.0 * (1 << 20) &&
+        gram_fused_shape(m, 32, p->gram_fused_max, &sh32))
+      sub_max = 32;
+  }
   auto sub_width = [&](int64_t kk) -> int64_t {
     if (kk >= kcap) return 0;
     const int64_t be = std::min((kk / b) * b + b, kcap);
-    return std::min<int64_t>(kMaxBlock, be - kk);
+    return std::min<int64_t>(sub_max, be - kk);
   };
   // Work credited to a stage for the sub-block that starts at column col,
   // taken back after the run if the run stopped before that sub-block (a
@@ -473,11 +493,19 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   // the compute units takes too many slots from the update it runs beside.
   // Power iterations need the whole updated trailing matrix before the
   // sample, so they run without it.
-  bool la = p->lookahead != 0 && power == 0 && panel_alg(p, b0) == kPanelGrid && kcap > b0;
+  // Blocks of at most 32 columns take their panels from the Gram matrix
+  // (la_gram); wider ones column by column.
+  const int alg0 = panel_alg(p, b0);
+  const bool la_gram = alg0 == kPanelGram && pad16(b0) <= 32;
+  bool la = p->lookahead != 0 && power == 0 && kcap > b0 && (alg0 == kPanelGrid || la_gram);
+  // The shape of the look-ahead panel of a sub-block (mr rows, width bb).
+  auto la_shape = [&](int64_t mr, int64_t bb, PanelShape* sh) -> bool {
+    if (la_gram) return gram_fused_shape(mr, (int)bb, p->gram_fused_max, sh);
+    return panel_shape(mr, (int)bb, p->num_cus, p->panel_target, sh) && sh->G <= p->num_cus / 4;
+  };
   if (la) {
     PanelShape sh1;
-    la = panel_shape(m - b0, (int)sub_width(b0), p->num_cus, p->panel_target, &sh1) &&
-         sh1.G <= p->num_cus / 4;
+    la = la_shape(m - b0, sub_width(b0), &sh1);
   }
   int64_t k = 0;
   int64_t yoff = 0;          // row offset of the next sample in the slabs
@@ -695,8 +723,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       const int64_t mpn = mp - bi;
       const int bpn = pad16(b_next);
       PanelShape shn;
-      if (!panel_shape(mpn, (int)b_next, p->num_cus, p->panel_target, &shn))
-        return RRF_ERR_SHAPE;
+      if (!la_shape(mpn, b_next, &shn)) return RRF_ERR_SHAPE;
       const double gby = e * mp * b_next * ysplits + 8.0 * mp * b_next;
       RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, gby,
                  launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
@@ -742,10 +769,12 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     ua.W = (T*)p->W; ua.ldw = bp; ua.Om = Om; ua.ldo = kOmLd; ua.qp = q_s;
     ua.P = Yp; ua.ldp = ldb; ua.split_stride = ldb * 64; ua.s0 = bi;
     ua.normpart = p->normpart;
-    const bool fused = panel_ready && update_panel_supported(bp, q_s, pan_shape);
+    const bool fused = panel_ready && (la_gram ? update_gram_supported(bp, q_s, pan_shape)
+                                               : update_panel_supported(bp, q_s, pan_shape));
     int su0 = upd_splits(mp, n, p->num_cus);
     if (fused) {
-      const int occ = update_panel_occupancy<T>(pan_shape);
+      const int occ = la_gram ? update_gram_occupancy<T>(pan_shape)
+                              : update_panel_occupancy<T>(pan_shape);
       if (occ > 0)
         su0 = upd_splits_fused(mp, n, (int64_t)occ * p->num_cus - pan_shape.G);
     }
@@ -755,7 +784,16 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     const double upd_flops = 2.0 * mp * n * bi + smp_flops;
     if (panel_ready) {
       pan.epoch_base = next_epoch(p);
-      if (fused) {
+      if (fused && la_gram) {
+        GramPanelArgs ga{};
+        ga.p = pan;
+        ga.part = p->gx;
+        ga.sums = p->gx + kGramPartWords;
+        RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops + pan_flops,
+                   2.0 * e * mp * n + pan_bytes,
+                   launch_update_gram<T>(ua, su, ga, pan_shape, s));
+        spec(RRF_STAGE_UPDATE, k_next, pan_flops, pan_bytes);
+      } else if (fused) {
         RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops + pan_flops,
                    2.0 * e * mp * n + pan_bytes,
                    launch_update_panel<T>(ua, su, pan, pan_shape, s));
@@ -764,7 +802,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
         RRF_LAUNCH(p, RRF_STAGE_UPDATE, upd_flops, 2.0 * e * mp * n,
                    launch_update<T>(ua, su, s));
         RRF_LAUNCH(p, RRF_STAGE_PANEL, pan_flops, pan_bytes,
-                   run_panel(p, pan, kPanelGrid, pan_shape, s));
+                   run_panel(p, pan, la_gram ? kPanelGram : kPanelGrid, pan_shape, s));
         spec(RRF_STAGE_PANEL, k_next, pan_flops, pan_bytes);
       }
     } else {
@@ -1093,10 +1131,11 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   p->lookahead = 1;
   if (const char* la = std::getenv("RRF_LOOKAHEAD")) p->lookahead = std::atoi(la) != 0;
   // RRF_PANEL selects the panel algorithm: "grid" (column by column, one
-  // grid-wide reduction per column; the only one the look-ahead overlaps),
-  // "gram" (the same reflectors from the Gram matrix, one grid exchange per
-  // sweep of columns), "tsqr" (tall-skinny QR with Householder
-  // reconstruction); the default picks gram or grid by the block width.
+  // grid-wide reduction per column), "gram" (the same reflectors from the
+  // Gram matrix, one grid exchange per sweep of columns), "tsqr" (tall-skinny
+  // QR with Householder reconstruction); the default picks gram or grid by
+  // the block width.  The look-ahead overlaps grid panels and, for blocks of
+  // at most 32 columns, gram panels.
   p->panel_mode = kPanelAuto;
   if (const char* pm = std::getenv("RRF_PANEL")) {
     if (std::strcmp(pm, "tsqr") == 0) p->panel_mode = kPanelTsqr;
@@ -1108,6 +1147,24 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
                             p->device) != hipSuccess) {
     free_plan(p);
     return RRF_ERR_HIP;
+  }
+  // Workgroups the Gram panel may hold inside the update's launch (the
+  // look-ahead of blocks of at most 32 columns): half the compute units, so
+  // that 4096-row panels take 4 rows per thread (its exchange is one per
+  // sweep, so a wider grid costs little; at 4096 x 4096 fp32, b = 32, 128
+  // workgroups measured 17.6 ms per run against 17.8 ms for 64 and 18.3 ms
+  // for 32); RRF_LA_GRAM_WGS overrides.
+  p->gram_fused_max = std::max(1, p->num_cus / 2);
+  // Sub-blocks of at most RRF_SUBBLOCK (16, 32 or 64) columns; by default
+  // chosen per run from the matrix size (run_impl).
+  p->sub_max = 0;
+  if (const char* sb = std::getenv("RRF_SUBBLOCK")) {
+    const int v = std::atoi(sb);
+    if (v == 16 || v == 32 || v == 64) p->sub_max = v;
+  }
+  if (const char* gw = std::getenv("RRF_LA_GRAM_WGS")) {
+    const int v = std::atoi(gw);
+    if (v >= 1 && v <= kMaxGramWGs) p->gram_fused_max = v;
   }
   // RRF_TEST_SPIN_LIMIT sets the poll rounds of every grid-wide wait of the
   // plan (tests: 0 makes each wait give up at its first poll, so the

@@ -13,8 +13,13 @@
 // look-ahead sample S_1 = A Omega_1 are independent: the same launch shape
 // runs them together (SAMPLE_ONLY: the non-panel workgroups only sample,
 // update_body with no reflectors and no store).
+//
+// Blocks of at most 32 columns take the panel from its Gram matrix (one
+// exchange per sweep of columns instead of one per column) in the same
+// arrangement: update_gram_kernel's first G workgroups run panel_gram_body.
 
 #include "panel_body.h"
+#include "panel_gram_body.h"
 #include "update_body.h"
 
 namespace rrf {
@@ -33,6 +38,64 @@ __global__ __launch_bounds__(256, 2) void update_panel_kernel(UpdateArgs<T> ua,
     update_body<T, 0, BP, false>(ua, t % nrb, t / nrb, nrb);
   else
     update_body<T, BP, BP, true>(ua, t % nrb, t / nrb, nrb);
+}
+
+template <typename T, int BP, int RPT>
+__global__ __launch_bounds__(256, 2) void update_gram_kernel(UpdateArgs<T> ua,
+                                                             GramPanelArgs ga,
+                                                             unsigned nrb) {
+  if ((int)blockIdx.x < ga.p.G) {
+    panel_gram_body<BP, RPT, 256>(ga, (int)blockIdx.x);
+    return;
+  }
+  const unsigned t = blockIdx.x - (unsigned)ga.p.G;
+  update_body<T, BP, BP, true>(ua, t % nrb, t / nrb, nrb);
+}
+
+// Rows per thread the Gram body accepts at 256 threads: whole staged chunks
+// of BP rows (BP^2 / 256 register slots each) and at least BP rows per
+// workgroup; at most 16, beyond which the body no longer fits the update's
+// register budget (two workgroups per compute unit) without spilling.
+constexpr int kUgMaxRpt = 16;
+template <int BP, int RPT>
+constexpr bool ug_built() {
+  return (BP == 16 || BP == 32) && RPT <= kUgMaxRpt && RPT % (BP * BP / 256) == 0 &&
+         (256 / BP) * RPT >= BP;
+}
+
+template <typename T, int BP, int RPT>
+hipError_t ug_go(const UpdateArgs<T>& ua, int nsplit, const GramPanelArgs& ga,
+                 hipStream_t s) {
+  const unsigned nrb = (unsigned)ceil_div(ua.mr, kUpdRows);
+  const dim3 grid((unsigned)ga.p.G + nrb * (unsigned)nsplit);
+  hipLaunchKernelGGL((update_gram_kernel<T, BP, RPT>), grid, dim3(256), 0, s, ua, ga, nrb);
+  return hipGetLastError();
+}
+
+template <typename T, int BP, int RPT>
+int ug_occ() {
+  static const int occ = [] {
+    int o = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &o, reinterpret_cast<const void*>(update_gram_kernel<T, BP, RPT>), 256, 0) != hipSuccess)
+      o = 0;
+    return o;
+  }();
+  return occ;
+}
+
+// Dispatch over rows per thread: go(integral_constant<RPT>) for a built
+// shape, else fallback.
+template <int BP, typename F, typename R>
+R ug_rpt(int rpt, F&& go, R fallback) {
+  switch (rpt) {
+    case 4: if constexpr (ug_built<BP, 4>()) return go(std::integral_constant<int, 4>{}); break;
+    case 8: if constexpr (ug_built<BP, 8>()) return go(std::integral_constant<int, 8>{}); break;
+    case 16: if constexpr (ug_built<BP, 16>()) return go(std::integral_constant<int, 16>{}); break;
+    case 32: if constexpr (ug_built<BP, 32>()) return go(std::integral_constant<int, 32>{}); break;
+    case 64: if constexpr (ug_built<BP, 64>()) return go(std::integral_constant<int, 64>{}); break;
+  }
+  return fallback;
 }
 
 // The sample-only form is built for 64-column panels, the width that takes
@@ -155,6 +218,45 @@ hipError_t launch_update_panel(const UpdateArgs<T>& ua, int nsplit,
   }
   return hipErrorNotSupported;
 }
+
+bool update_gram_supported(int bp, int qp, const PanelShape& sh) {
+  if (bp <= 0 || bp != qp || bp != sh.bp || sh.G < 1 || sh.G > kMaxGramWGs) return false;
+  if (sh.bp == 16) return ug_rpt<16>(sh.rpt, [](auto) { return true; }, false);
+  if (sh.bp == 32) return ug_rpt<32>(sh.rpt, [](auto) { return true; }, false);
+  return false;
+}
+
+template <typename T>
+int update_gram_occupancy(const PanelShape& sh) {
+  if (sh.bp == 16)
+    return ug_rpt<16>(sh.rpt, [](auto r) { return ug_occ<T, 16, decltype(r)::value>(); }, 0);
+  if (sh.bp == 32)
+    return ug_rpt<32>(sh.rpt, [](auto r) { return ug_occ<T, 32, decltype(r)::value>(); }, 0);
+  return 0;
+}
+
+template int update_gram_occupancy<float>(const PanelShape&);
+template int update_gram_occupancy<double>(const PanelShape&);
+
+template <typename T>
+hipError_t launch_update_gram(const UpdateArgs<T>& ua, int nsplit, const GramPanelArgs& ga,
+                              const PanelShape& sh, hipStream_t s) {
+  if (!update_gram_supported(ua.bp, ua.qp, sh) || !ua.dst || ua.mr <= 0 || ua.n <= 0 ||
+      ga.p.G != sh.G || ga.p.b < 1 || ga.p.b > sh.bp)
+    return hipErrorNotSupported;
+  // 32-bit buffer offsets, as in launch_update.
+  const int64_t ld = std::max(ua.lds, ua.ldd);
+  if (ld < ua.mr || (int64_t)kUpdChunk * ld * (int64_t)sizeof(T) > ((int64_t)1 << 30))
+    return hipErrorInvalidValue;
+  if (sh.bp == 16)
+    return ug_rpt<16>(sh.rpt, [&](auto r) { return ug_go<T, 16, decltype(r)::value>(ua, nsplit, ga, s); },
+                      hipErrorNotSupported);
+  return ug_rpt<32>(sh.rpt, [&](auto r) { return ug_go<T, 32, decltype(r)::value>(ua, nsplit, ga, s); },
+                    hipErrorNotSupported);
+}
+
+template hipError_t launch_update_gram<float>(const UpdateArgs<float>&, int, const GramPanelArgs&, const PanelShape&, hipStream_t);
+template hipError_t launch_update_gram<double>(const UpdateArgs<double>&, int, const GramPanelArgs&, const PanelShape&, hipStream_t);
 
 template hipError_t launch_update_panel<float>(const UpdateArgs<float>&, int, const PanelArgs&, const PanelShape&, hipStream_t);
 template hipError_t launch_update_panel<double>(const UpdateArgs<double>&, int, const PanelArgs&, const PanelShape&, hipStream_t);

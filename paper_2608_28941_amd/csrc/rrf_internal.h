@@ -223,6 +223,18 @@ hipError_t launch_sample_panel(const UpdateArgs<T>& ua, int nsplit,
                                hipStream_t s);
 template <typename T>
 int sample_panel_occupancy(const PanelShape& sh);
+// Look-ahead for blocks of at most 32 columns: the update and the next
+// block's Gram panel (256 threads per workgroup) in one launch; supported
+// when bp == qp == the panel's padded width (16 or 32).
+bool update_gram_supported(int bp, int qp, const PanelShape& sh);
+template <typename T>
+hipError_t launch_update_gram(const UpdateArgs<T>& ua, int nsplit, const GramPanelArgs& ga,
+                              const PanelShape& sh, hipStream_t s);
+template <typename T>
+int update_gram_occupancy(const PanelShape& sh);
+// Shape of a Gram panel inside that launch: the fewest rows per thread whose
+// grid has at most max_wgs workgroups.
+bool gram_fused_shape(int64_t m, int b, int max_wgs, PanelShape* out);
 // Ysum[r + k * ldy] = sum_s P_s[r + k * ldp] for r < m, k < b; 0 elsewhere
 // for r < rows_pad, k < bp (binary64).
 template <typename T>

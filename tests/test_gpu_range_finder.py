@@ -105,9 +105,20 @@ SCALED = [
 
 @pytest.mark.parametrize("name,m,n,b,tol", SCALED)
 def test_scaled_workloads(name, m, n, b, tol):
-    # Element by element: with b = 64 and 48 this is the look-ahead path
+    # Element by element, in the default configuration: the look-ahead with
+    # the Gram panel inside the update's launch (blocks of b > 32 columns of
+    # these small matrices run as 32-column sub-blocks).
+    w = W.scaled(name, m, n, block_b=b, tol=tol)
+    _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
+
+
+@pytest.mark.parametrize("name,m,n,b,tol", [SCALED[1], SCALED[2], SCALED[5]])
+def test_scaled_workloads_64_column_subblocks(monkeypatch, name, m, n, b, tol):
+    # Element by element with 64-column sub-blocks (the width large matrices
+    # take, e.g. 16384 x 16384): the column-by-column look-ahead path
     # (update_panel_kernel with its fused sample, the redundant panel update
     # in thin_apply_kernel, block 0's panel beside the first sample).
+    monkeypatch.setenv("RRF_SUBBLOCK", "64")
     w = W.scaled(name, m, n, block_b=b, tol=tol)
     _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
 
@@ -120,10 +131,12 @@ def test_scaled_workloads_tsqr_panel(monkeypatch, name, m, n, b, tol):
     _check_against_live_oracle(w, W.build_matrix(w))
 
 
-@pytest.mark.parametrize("name,m,n,b,tol", [SCALED[1], SCALED[2], SCALED[5]])
+@pytest.mark.parametrize("name,m,n,b,tol", [SCALED[0], SCALED[1], SCALED[2], SCALED[3],
+                                            SCALED[4], SCALED[5]])
 def test_scaled_workloads_without_lookahead(monkeypatch, name, m, n, b, tol):
-    # Same bar with the look-ahead off (b = 64 and 48: every panel in its own
-    # launch, no redundant panel update, no block-0 sample/panel launch).
+    # Same bar with the look-ahead off (every panel in its own launch, no
+    # redundant panel update, no block-0 sample/panel launch; b <= 32: the
+    # Gram panel, queued during the stop test).
     monkeypatch.setenv("RRF_LOOKAHEAD", "0")
     w = W.scaled(name, m, n, block_b=b, tol=tol)
     _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
@@ -199,19 +212,56 @@ def test_lookahead_tall_panel_elementwise(monkeypatch, lookahead):
     # rows per thread (panels above 8192 rows); k = 320 in five blocks,
     # E / sigma^2 = 3.0 at k = 256 and 0.17 at 320.
     monkeypatch.setenv("RRF_LOOKAHEAD", lookahead)
+    monkeypatch.setenv("RRF_SUBBLOCK", "64")
     w = W.scaled("square_fp64_16384", 12288, 384, block_b=64, tol=1e-2)
     _, _, k, _ = _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
     assert k == 320
 
 
+@pytest.mark.parametrize("name,m,n,b,tol,wgs", [
+    ("galore_fp32_4096x4096", 1024, 1024, 32, None, 64),   # 4 rows per thread, 32 workgroups
+    ("galore_fp32_4096x4096", 1024, 1024, 32, None, 16),   # 8 rows per thread
+    ("galore_fp32_4096x4096", 1024, 1024, 32, None, 8),    # 16 rows per thread
+    ("tall_fp64_131072x2048", 8192, 256, None, None, 64),  # 16 rows per thread, 64 workgroups
+    ("tiny_fp64_500x300", 500, 300, 16, 1e-4, 64),         # 16 columns, 4 rows per thread
+    ("tiny_fp64_500x300", 500, 300, 16, 1e-4, 4),          # 8 rows per thread
+    ("tiny_fp64_500x300", 500, 300, 16, 1e-4, 2),          # 16 rows per thread
+    ("tiny_fp64_500x300", 333, 250, 20, 1e-5, 64),         # 20 of 32 columns, ragged
+])
+def test_lookahead_gram_panel_shapes(monkeypatch, name, m, n, b, tol, wgs):
+    # Blocks of at most 32 columns: the next block's Gram panel runs on the
+    # first workgroups of the update's launch; RRF_LA_GRAM_WGS caps its grid,
+    # which picks the rows per thread.  Element by element against the
+    # oracle.
+    monkeypatch.setenv("RRF_LA_GRAM_WGS", str(wgs))
+    w = W.scaled(name, m, n, block_b=b, tol=tol)
+    _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
+
+
+def test_deterministic_repeat_lookahead_gram():
+    # Bit-identical results from two runs of the Gram look-ahead path (b = 32).
+    w = W.scaled("tall_fp64_131072x2048", 8192, 256)
+    A = to_dev(W.build_matrix(w))
+    with rrf.Plan(torch.float64, 8192, 256, 32) as p:
+        Q1, B1, k1 = p.run(A, w.tol, 32, w.sketch_seed)
+        Q2, B2, k2 = p.run(A, w.tol, 32, w.sketch_seed)
+        torch.cuda.synchronize()
+        assert k1 == k2 and k1 > 32
+        assert torch.equal(Q1, Q2) and torch.equal(B1, B2)
+
+
+@pytest.mark.parametrize("sub", ["64", "auto"])
 @pytest.mark.parametrize("name,m,n,b,tol", [
     ("square_fp64_16384", 2048, 2048, 128, 1e-5),    # two 64-column sub-blocks
     ("tiny_fp64_500x300", 333, 250, 100, 1e-5),      # sub-blocks of 64 and 36
     ("galore_fp32_4096x4096", 1024, 1024, 80, 2e-2), # 64 and 16: mixed panel routes
 ])
-def test_blocks_wider_than_64(name, m, n, b, tol):
-    # block_b > 64 runs as sub-blocks of at most 64 columns with the stop
-    # test at block ends; the oracle factors each block whole.
+def test_blocks_wider_than_64(monkeypatch, name, m, n, b, tol, sub):
+    # block_b > 64 runs as sub-blocks of at most 64 columns (32 for these
+    # small matrices by default) with the stop test at block ends; the oracle
+    # factors each block whole.
+    if sub != "auto":
+        monkeypatch.setenv("RRF_SUBBLOCK", sub)
     w = W.scaled(name, m, n, block_b=b, tol=tol)
     _, _, k, ref = _check_against_live_oracle(w, W.build_matrix(w), elementwise=True)
     assert k % b == 0 or k == min(m, n)
@@ -239,8 +289,10 @@ def test_panel_beyond_register_capacity():
     assert orth_err(Q) <= ORTH_TOL[np.dtype(np.float64)]
 
 
-def test_deterministic_repeat_lookahead():
-    # Bit-identical results from two runs of the look-ahead path (b = 64).
+def test_deterministic_repeat_lookahead(monkeypatch):
+    # Bit-identical results from two runs of the look-ahead path (b = 64,
+    # 64-column sub-blocks).
+    monkeypatch.setenv("RRF_SUBBLOCK", "64")
     w = W.scaled("square_fp64_16384", 2048, 2048, tol=1e-5)
     A = to_dev(W.build_matrix(w))
     with rrf.Plan(torch.float64, 2048, 2048, 64) as p:
