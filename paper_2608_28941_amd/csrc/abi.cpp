@@ -33,7 +33,7 @@ namespace {
 
 constexpr int kMaxUpdSplits = 8;
 constexpr int kMaxRedSplits = 32;
-constexpr int kOmLd = 64;         // Omega stored [c][q] with row length 64
+constexpr int kOmLd = 256;        // Omega stored [c][q]: a batch of 256 sketch columns
 constexpr int kPanelGrid = 0;      // column-by-column panel, one grid reduction per column
 constexpr int kPanelTsqr = 1;      // tall-skinny QR + Householder reconstruction
 constexpr int kPanelGram = 2;      // column recurrence from the Gram matrix, one exchange per sweep
@@ -452,17 +452,37 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     p->spec.push_back(SpecWork{stage, col, fl, by});
   };
 
+  // Sketch columns are generated kOmLd at a time: Om holds the global
+  // columns [om_k0, om_k0 + kOmLd) (row-major, rows padded with zeros to the
+  // update's chunk), and a batch is generated when a sample needs a column
+  // window beyond the one held (one launch per batch of sub-blocks instead
+  // of one per sub-block).  Columns of a window past the sample's width are
+  // other sketch columns; the sample's unused columns are never read.
+  int64_t om_k0 = -1;
+  auto sketch_window = [&](int64_t col, int qp, T** win) -> rrf_status {
+    if (om_k0 < 0 || col < om_k0 || col + qp > om_k0 + kOmLd) {
+      const int64_t nc = std::min<int64_t>(kOmLd, kcap - col);
+      RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * nc,
+                 launch_sketch<T>(seed, n, round_up(n, kUpdChunk), col, nc, Om, kOmLd, 1, s));
+      spec(RRF_STAGE_SKETCH, col, 0.0, e * n * nc);
+      om_k0 = col;
+    }
+    *win = Om + (col - om_k0);
+    return RRF_OK;
+  };
+
   // Initial sample Y_0 = A Omega_0 and ||A||_F^2 in one read of A.
   const int64_t b0 = sub_width(0);
   const int q0 = b0 > 0 ? pad16(b0) : 0;
-  if (b0 > 0)
-    RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b0,
-               launch_sketch<T>(seed, n, round_up(n, kUpdChunk), 0, b0, Om,
-                                kOmLd, 1, s));
+  T* om_win = Om;
+  if (b0 > 0) {
+    rrf_status rs = sketch_window(0, q0, &om_win);
+    if (rs != RRF_OK) return rs;
+  }
   UpdateArgs<T> u{};
   u.src = A; u.lds = lda; u.dst = nullptr; u.ldd = 0; u.mr = m; u.n = n;
   u.V = nullptr; u.ldv = 0; u.bp = 0; u.W = nullptr; u.ldw = 0;
-  u.Om = Om; u.ldo = kOmLd; u.qp = q0; u.P = Yp; u.ldp = ldb;
+  u.Om = om_win; u.ldo = kOmLd; u.qp = q0; u.P = Yp; u.ldp = ldb;
   u.split_stride = ldb * 64; u.s0 = 0; u.normpart = p->normpart;
   {
     const int su0 = upd_splits(m, n, p->num_cus);
@@ -656,11 +676,10 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
         // look-ahead sample S_1 = A Omega_1 (independent of it) in one
         // launch.  The gather above has already read the partials of Y_0
         // that S_1 replaces.
-        RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
-                   launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_next, b_next,
-                                    Om, kOmLd, 1, s));
-        spec(RRF_STAGE_SKETCH, k_next, 0.0, e * n * b_next);
+        rrf_status rs = sketch_window(k_next, 64, &om_win);
+        if (rs != RRF_OK) return rs;
         UpdateArgs<T> u1 = u;
+        u1.Om = om_win;
         u1.qp = 64;
         u1.normpart = nullptr;
         const int su1 = upd_splits_fused(m, n, (int64_t)occ0 * p->num_cus - sh.G);
@@ -692,11 +711,10 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     // panel above (later sub-blocks get their look-ahead sample from the
     // previous update).
     if (la && sub == 0 && b_next > 0 && !s1_done) {
-      RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_next,
-                 launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_next, b_next,
-                                  Om, kOmLd, 1, s));
-      spec(RRF_STAGE_SKETCH, k_next, 0.0, e * n * b_next);
+      rrf_status rs = sketch_window(k_next, pad16(b_next), &om_win);
+      if (rs != RRF_OK) return rs;
       UpdateArgs<T> u1 = u;
+      u1.Om = om_win;
       u1.qp = pad16(b_next);
       u1.normpart = nullptr;
       const double sfl = 2.0 * m * n * b_next, sby = e * (m * n + m * b_next);
@@ -756,17 +774,15 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     const int64_t b_s = (la ? b_next > 0 : true) ? sub_width(k_s) : 0;
     const int q_s = b_s > 0 ? pad16(b_s) : 0;
     if (b_s > 0) {
-      RRF_LAUNCH(p, RRF_STAGE_SKETCH, 0.0, e * n * b_s,
-                 launch_sketch<T>(seed, n, round_up(n, kUpdChunk), k_s, b_s, Om,
-                                  kOmLd, 1, s));
-      spec(RRF_STAGE_SKETCH, k_s, 0.0, e * n * b_s);
+      rrf_status rs = sketch_window(k_s, q_s, &om_win);
+      if (rs != RRF_OK) return rs;
     }
 
     // B[k:m, :] -= V_i W, fused with the sample and the norms.
     UpdateArgs<T> ua{};
     ua.src = src + k; ua.lds = lsrc; ua.dst = Bws + k; ua.ldd = ldb;
     ua.mr = mp; ua.n = n; ua.V = V + k + k * ldb; ua.ldv = ldb; ua.bp = bp;
-    ua.W = (T*)p->W; ua.ldw = bp; ua.Om = Om; ua.ldo = kOmLd; ua.qp = q_s;
+    ua.W = (T*)p->W; ua.ldw = bp; ua.Om = om_win; ua.ldo = kOmLd; ua.qp = q_s;
     ua.P = Yp; ua.ldp = ldb; ua.split_stride = ldb * 64; ua.s0 = bi;
     ua.normpart = p->normpart;
     const bool fused = panel_ready && (la_gram ? update_gram_supported(bp, q_s, pan_shape)

@@ -13,7 +13,9 @@
 //   3. every workgroup forms W = T^T Z (the same values everywhere) and
 //      updates its rows, Y_w -= V_w W, in the transposed MFMA frame (16
 //      consecutive rows per lane group: coalesced loads and stores).
-// The exchange uses the epoch-tagged words of the panel kernels (xchg.h).
+// The exchange uses the epoch-tagged words of the panel kernels (xchg.h),
+// and carries only the 16 x 16 tiles of Z that the block has: ceil(b / 16)
+// x ceil(ncols / 16) of the 4 x 4 (4 of 16 at b = ncols = 32).
 
 #include "mfma.h"
 #include "xchg.h"
@@ -21,7 +23,7 @@
 namespace rrf {
 namespace {
 
-constexpr int kThinSlots = 16 * 256;   // 64 x 64 values in MFMA tile order
+constexpr int kThinSlots = 16 * 256;   // 64 x 64 values in MFMA tile order (at most)
 
 // Rows of a chunk staged in LDS (V and Y, 64 columns each).
 constexpr int kThinChunk = 64;
@@ -39,6 +41,10 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
   const int64_t r_end = min(a.mr, r_begin + a.rows_per_wg);
   const unsigned epoch = a.epoch_base + 1u;
   const bool forced = waits_forced(a.st);
+  // Exchanged tiles: PT row tiles (reflectors) x CT column tiles, slot
+  // ((pt CT + ct) 4 + i) 64 + lane; NS slots in all (uniform).
+  const int PT = (min(a.b, 64) + 15) / 16, CT = (min(a.ncols, 64) + 15) / 16;
+  const int NS = PT * CT * 256;
 
   // T (leading b x b block, upper triangular) to LDS: all loads issued
   // before the first use (columns past b read column 0), entries outside the
@@ -98,20 +104,22 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
         acc[ct] = Mfma<double>::op(av, Ys[4 * s4 + l16][16 * ct + m16], acc[ct]);
     }
   }
-  {
-    u64* dst = a.part + (int64_t)w * kThinSlots * 2;
+  if (wv < PT) {
+    u64* dst = a.part + (int64_t)w * NS * 2;
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct)
+      if (ct < CT) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        put_tagged(&dst[(((wv * 4 + ct) * 4 + i) * 64 + lane) * 2], acc[ct][i], epoch);
+        for (int i = 0; i < 4; ++i)
+          put_tagged(&dst[(((wv * CT + ct) * 4 + i) * 64 + lane) * 2], acc[ct][i], epoch);
+      }
   }
   // 2. This workgroup's slice of Z, summed over all workgroups in a fixed
   //    order (nsub threads per entry, then in LDS).
   {
-    const int se = (kThinSlots + G - 1) / G;
+    const int se = (NS + G - 1) / G;
     const int e0 = w * se;
-    const int ne = max(0, min(kThinSlots, e0 + se) - e0);
+    const int ne = max(0, min(NS, e0 + se) - e0);
     const int nsub = max(1, min(16, 256 / max(ne, 1)));
     const int per = 256 / nsub;
     for (int p0 = 0; p0 < ne; p0 += per) {
@@ -127,7 +135,7 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
               const int ww = w0 + u * nsub;
-              const u64* q = src + (int64_t)(ww < G ? ww : 0) * kThinSlots * 2;
+              const u64* q = src + (int64_t)(ww < G ? ww : 0) * NS * 2;
               hi[u] = get_word(q);
               lo[u] = get_word(q + 1);
             }
@@ -150,17 +158,19 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
       __syncthreads();
     }
   }
-  // 3. Every workgroup reads all of Z: slot ((pt 4 + ct) 4 + i) 64 + lane
-  //    holds Z[16 pt + lane/16 + 4 i][16 ct + lane%16].
+  // 3. Every workgroup reads all of Z: slot ((pt CT + ct) 4 + i) 64 + lane
+  //    holds Z[16 pt + lane/16 + 4 i][16 ct + lane%16]; tiles not exchanged
+  //    are zero (reflectors >= b and columns >= ncols contribute nothing).
   {
     constexpr int NPT = kThinSlots / 256;
+    const int nq = NS / 256;
     u64 hi[NPT], lo[NPT];
     unsigned spins = 0;
     bool ok;
     do {
 #pragma unroll
       for (int i = 0; i < NPT; ++i) {
-        const u64* q = a.sums + (int64_t)(t + 256 * i) * 2;
+        const u64* q = a.sums + (int64_t)(t + 256 * (i < nq ? i : 0)) * 2;
         hi[i] = get_word(q);
         lo[i] = get_word(q + 1);
       }
@@ -172,8 +182,15 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
     for (int i = 0; i < NPT; ++i) {
       const int e = t + 256 * i;
       const int ln = e % 64, it = (e / 64) % 4, tile = e / 256;
-      const int pt = tile / 4, ct = tile % 4;
-      ZW[16 * pt + ln / 16 + 4 * it][16 * ct + ln % 16] = untag(hi[i], lo[i]);
+      if (i < nq) {
+        const int pt = tile / CT, ct = tile % CT;
+        ZW[16 * pt + ln / 16 + 4 * it][16 * ct + ln % 16] = untag(hi[i], lo[i]);
+      }
+    }
+    // Tiles outside PT x CT.
+    for (int e = t; e < 4096; e += 256) {
+      const int r = e / 64, c = e % 64;
+      if (r >= 16 * PT || c >= 16 * CT) ZW[r][c] = 0.0;
     }
   }
   __syncthreads();
@@ -231,8 +248,8 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
 }  // namespace
 
 hipError_t launch_thin_apply(ThinApplyArgs a, int num_cus, hipStream_t s) {
-  if (a.mr <= 0) return hipSuccess;
-  if (a.b < 1 || a.b > 64) return hipErrorInvalidValue;
+  if (a.mr <= 0 || a.ncols <= 0) return hipSuccess;
+  if (a.b < 1 || a.b > 64 || a.ncols > 64) return hipErrorInvalidValue;
   int occ = 0;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
       &occ, reinterpret_cast<const void*>(thin_apply_kernel), 256, 0);
