@@ -44,10 +44,11 @@ struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
-      rowj, st, trace, tsqr, gx, tx, Yest, spec, Tpow;
+      rowj, st, trace, tsqr, gx, tx, Yest, spec, Tpow, Tp, pairs;
   size_t total() const {
     return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
-           normpart + red + rowj + st + trace + tsqr + gx + tx + Yest + spec + Tpow;
+           normpart + red + rowj + st + trace + tsqr + gx + tx + Yest + spec + Tpow +
+           Tp + pairs;
   }
 };
 
@@ -86,6 +87,10 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.Yest = (size_t)z.ldysum * 64 * 8;
   z.spec = (size_t)kMaxSpecWGs * 4096 * 8;
   z.Tpow = (size_t)64 * 64 * 8;
+  // Explicit-Q pass: merged T of block pairs (laid out like T) and the pair
+  // list (pairs of blocks of at least 16 columns).
+  z.Tp = z.Tm;
+  z.pairs = (size_t)(z.kcols / 32 + 2) * sizeof(OrgqrPair);
   // Tall-skinny QR panel: the largest tree over the block widths the plan
   // allows (the tree shrinks with the panel's rows).
   z.tsqr = 8;
@@ -117,6 +122,9 @@ struct rrf_plan {
   std::vector<void*> dev_allocs;
   void *Bws, *Ypart, *Om, *Zpart, *W, *Q, *Q64;
   double* tsqr;              // scratch of the tall-skinny QR panel
+  double* Tp;                // merged T of block pairs (explicit-Q pass)
+  OrgqrPair* pairs_d;        // pair list, device
+  OrgqrPair* pairs_h;        // pair list, pinned host staging
   int panel_mode;            // kPanelGrid, kPanelTsqr, kPanelGram or kPanelAuto
   double *V, *Tm, *tau, *Ysum;
   double *normpart, *trace_trail_d, *trace_sub_d, *trace_spec_d;
@@ -168,6 +176,7 @@ void free_plan(rrf_plan* p) {
   for (void* q : p->dev_allocs) (void)hipFree(q);
   p->dev_allocs.clear();
   if (p->st_host) (void)hipHostFree(p->st_host);
+  if (p->pairs_h) (void)hipHostFree(p->pairs_h);
   for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
   if (p->state_ev) (void)hipEventDestroy(p->state_ev);
   if (p->map_c) (void)hipFree(p->map_c);
@@ -930,20 +939,55 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   p->nblocks = blk;
 
   // Explicit Q = H_0 ... H_{k-1} [I_k; 0], backward over the sub-blocks, in
-  // binary64 (float plans round the result once).
+  // binary64 (float plans round the result once).  Adjacent sub-blocks of
+  // 16 to 32 columns are applied in pairs, as one block of up to 64
+  // reflectors with their merged T (orgqr_pairs.hip): half the passes over Q
+  // for 32-column blocks.
   const int nsub = (int)p->sub_start.size();
   if (k > 0) {
     double* Qd = std::is_same<T, double>::value ? (double*)Q : (double*)p->Q64;
     RRF_LAUNCH(p, RRF_STAGE_ORGQR, 0.0, 8.0 * m * k,
                launch_fill_identity<double>(Qd, ldb, m, k, s));
-    for (int i = nsub - 1; i >= 0; --i) {
-      const int64_t ki = p->sub_start[i];
-      const int64_t bi = (i + 1 < nsub ? p->sub_start[i + 1] : k) - ki;
+    struct Group { int64_t k0, b; int pair; };   // pair: index into the pair list, or -1
+    std::vector<Group> groups;
+    int npairs = 0;
+    auto width = [&](int i) { return (i + 1 < nsub ? p->sub_start[i + 1] : k) - p->sub_start[i]; };
+    for (int i = nsub - 1; i >= 0;) {
+      const int64_t bi = width(i);
+      const int64_t bl = i >= 1 ? width(i - 1) : 0;
+      if (i >= 1 && bi >= 16 && bi <= 32 && bl >= 16 && bl <= 32 &&
+          (size_t)(npairs + 1) * sizeof(OrgqrPair) <= p->sz.pairs) {
+        p->pairs_h[npairs] = OrgqrPair{p->sub_start[i - 1], (int)bl, (int)bi};
+        groups.push_back(Group{p->sub_start[i - 1], bl + bi, npairs});
+        ++npairs;
+        i -= 2;
+      } else {
+        groups.push_back(Group{p->sub_start[i], bi, -1});
+        i -= 1;
+      }
+    }
+    if (npairs > 0) {
+      he = hipMemcpyAsync(p->pairs_d, p->pairs_h, npairs * sizeof(OrgqrPair),
+                          hipMemcpyHostToDevice, s);
+      if (he != hipSuccess) return hip_fail(he);
+      PairArgs pa{};
+      pa.pairs = p->pairs_d; pa.V = V; pa.ldv = ldb; pa.m = m;
+      pa.Tm = Tm; pa.ldt = kTLd; pa.Tp = p->Tp; pa.part = (double*)p->Zpart;
+      // Row splits of the V_1^T V_2 sums: about 512 rows each (tall panels
+      // need many workgroups per pair), within the partial buffer.
+      const int64_t cap = (int64_t)(p->sz.Zpart / 8) / (1024 * (int64_t)npairs);
+      pa.nsplit = (int)std::max<int64_t>(1, std::min<int64_t>({ceil_div(m, 512), 256, cap}));
+      RRF_LAUNCH(p, RRF_STAGE_ORGQR, 2.0 * m * 32 * 32 * npairs, 8.0 * m * 64 * npairs,
+                 launch_orgqr_pairs(pa, npairs, s));
+    }
+    for (const Group& gr : groups) {
+      const int64_t ki = gr.k0, bi = gr.b;
+      const double* Tg = gr.pair >= 0 ? p->Tp + ki * kTLd : Tm + ki * kTLd;
       if (k - ki <= 64) {
-        // The last sub-block's columns alone: the one-launch thin kernel.
+        // The last columns alone: the one-launch thin kernel.
         ThinApplyArgs ta{};
         ta.V = V + ki + ki * ldb; ta.ldv = ldb;
-        ta.Tm = Tm + ki * kTLd; ta.ldt = kTLd; ta.b = (int)bi; ta.trans = 0;
+        ta.Tm = Tg; ta.ldt = kTLd; ta.b = (int)bi; ta.trans = 0;
         ta.Y = Qd + ki + ki * ldb; ta.ldy = ldb; ta.mr = m - ki; ta.ncols = (int)(k - ki);
         ta.part = p->tx; ta.sums = p->tx + kThinPartWords;
         ta.epoch_base = next_epoch(p); ta.st = p->st;
@@ -952,9 +996,8 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
                    launch_thin_apply(ta, p->num_cus, s));
         continue;
       }
-      rrf_status rs = apply_wy<double>(p, 0, V + ki + ki * ldb, ldb,
-                                       Tm + ki * kTLd, kTLd, (int)bi, pad16(bi),
-                                       Qd + ki + ki * ldb, ldb, m - ki, k - ki,
+      rrf_status rs = apply_wy<double>(p, 0, V + ki + ki * ldb, ldb, Tg, kTLd, (int)bi,
+                                       pad16(bi), Qd + ki + ki * ldb, ldb, m - ki, k - ki,
                                        RRF_STAGE_ORGQR);
       if (rs != RRF_OK) return rs;
     }
@@ -1233,6 +1276,8 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   RRF_ALLOC(Yest, p->sz.Yest);
   RRF_ALLOC(spec_part, p->sz.spec);
   RRF_ALLOC(Tpow, p->sz.Tpow);
+  RRF_ALLOC(Tp, p->sz.Tp);
+  RRF_ALLOC(pairs_d, p->sz.pairs);
 #undef RRF_ALLOC
   if (e == hipSuccess) {
     ++counter;
@@ -1240,6 +1285,7 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
     if (f && std::atoi(f) == counter) e = hipErrorOutOfMemory;
     else e = hipHostMalloc((void**)&p->st_host, sizeof(DevState), 0);
   }
+  if (e == hipSuccess) e = hipHostMalloc((void**)&p->pairs_h, p->sz.pairs, 0);
   if (e == hipSuccess) e = hipMemsetAsync(p->red, 0, p->sz.red, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->rowj, 0, p->sz.rowj, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->gx, 0, p->sz.gx, p->stream);

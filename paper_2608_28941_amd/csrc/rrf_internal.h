@@ -183,6 +183,20 @@ struct GramPanelArgs {
 bool gram_panel_shape(int64_t m, int b, int num_cus, PanelShape* out);
 hipError_t launch_panel_gram(const GramPanelArgs& a, const PanelShape& sh, hipStream_t s);
 
+// Explicit-Q pass: two adjacent blocks of 16..32 reflectors each applied as
+// one block (orgqr_pairs.hip).  Per pair: k0, the first column, b1 and b2
+// the widths.  part holds npairs x nsplit x 32 x 32 doubles; the merged T
+// of the pair at column k0 goes to Tp + k0 ldt (64 x 64, ld ldt).
+struct OrgqrPair { int64_t k0; int b1, b2; };
+struct PairArgs {
+  const OrgqrPair* pairs;
+  double* V; int64_t ldv; int64_t m;
+  const double* Tm; int64_t ldt;
+  double* Tp;
+  double* part; int nsplit;
+};
+hipError_t launch_orgqr_pairs(const PairArgs& a, int npairs, hipStream_t s);
+
 // Y <- Y - V T^T (V^T Y) for a thin Y (mr x ncols, ncols <= 64), binary64,
 // one launch (reflectors p >= b and columns >= ncols are
 // treated as zero).  part: kMaxThinWGs x 4096 tagged values, sums: 4096;
