@@ -91,11 +91,12 @@ typedef enum rrf_stage {
  * rrf_plan_create -- allocate a plan and its device workspace.
  *   dtype        RRF_F32 or RRF_F64.
  *   m_max,n_max  largest A the plan will see (>= 1).
- *   block_b_max  largest block size b, 1 <= block_b_max <= 128.  A block wider
- *                than 64 columns runs as sub-blocks of 64 (the last one
- *                ragged): Householder QR is column by column, so the
- *                reflectors are the block's own; the stop test runs once per
- *                block.
+ *   block_b_max  largest block size b, 1 <= block_b_max <= 128.  A block runs
+ *                as sub-blocks of at most 64 columns (32 on matrices of at
+ *                most 512 MiB, where a narrow update beside a narrow panel
+ *                is faster; the last one ragged): Householder QR is column
+ *                by column, so the reflectors are the block's own; the stop
+ *                test runs once per block.
  *   k_max        rank cap (>= 0); 0 means min(m, n).  A cap below the rank the
  *                tolerance needs is the fixed-rank mode of Sec. 6 (Fig. 6).
  *   hip_stream   hipStream_t to enqueue on; NULL means the null stream.
@@ -115,6 +116,27 @@ typedef enum rrf_stage {
 rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
                            int64_t n_max, int64_t block_b_max, int64_t k_max,
                            void* hip_stream);
+
+/* ---------------------------------------------------------------------------
+ * rrf_plan_create_in -- rrf_plan_create with the device workspace provided
+ * by the caller (so that, e.g., a framework's allocator owns all device
+ * memory).  Same arguments as rrf_plan_create, plus:
+ *   workspace        device pointer, 256-byte aligned, at least
+ *                    workspace_bytes long; NULL behaves as rrf_plan_create.
+ *   workspace_bytes  >= rrf_workspace_size(dtype, m_max, n_max, block_b_max,
+ *                    k_max).
+ * The plan carves all of its device buffers from the workspace and frees
+ * none of it: the caller owns it, must keep it alive until rrf_destroy and
+ * must not touch it meanwhile (Q and B returned by rrf_run point into it).
+ * The plan still allocates small pinned host buffers (run state, pair list)
+ * and, on demand, the subspace map's partials (rrf_subspace_map).
+ * RRF_ERR_INVALID_ARG for a misaligned or short workspace (checked on the
+ * host before any device call); otherwise as rrf_plan_create.
+ * ------------------------------------------------------------------------- */
+rrf_status rrf_plan_create_in(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
+                              int64_t n_max, int64_t block_b_max, int64_t k_max,
+                              void* hip_stream, void* workspace,
+                              size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
  * rrf_run -- Alg. 2 on A, then explicit Q and B.
@@ -146,8 +168,9 @@ rrf_status rrf_destroy(rrf_plan_t plan);
 /* Static string for a status code; never NULL. */
 const char* rrf_status_string(rrf_status s);
 
-/* Device workspace in bytes that rrf_plan_create allocates for these maxima
- * (host-only computation; no GPU needed). */
+/* Device workspace in bytes that rrf_plan_create allocates for these maxima,
+ * and that rrf_plan_create_in needs (every buffer at a 256-byte boundary;
+ * host-only computation, no GPU needed). */
 rrf_status rrf_workspace_size(rrf_dtype dtype, int64_t m_max, int64_t n_max,
                               int64_t block_b_max, int64_t k_max,
                               size_t* bytes);

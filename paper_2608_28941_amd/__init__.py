@@ -68,7 +68,11 @@ class Plan:
     """A plan (workspace for maxima m_max x n_max, block <= block_b_max)."""
 
     def __init__(self, dtype, m_max, n_max, block_b_max=64, k_max=0,
-                 stream=None, device=None):
+                 stream=None, device=None, workspace=None):
+        """workspace: optional device tensor (any dtype, contiguous, 256-byte
+        aligned, at least workspace_size(...) bytes) that the plan carves its
+        device buffers from (rrf_plan_create_in); the plan keeps a reference
+        to it."""
         torch = _torch()
         self.dtype = dtype
         self.code = _dtype_code(dtype)
@@ -76,10 +80,21 @@ class Plan:
         self.stream = torch.cuda.current_stream(self.device) if stream is None else stream
         self.lib = _abi.load()
         h = ctypes.c_void_p()
-        st = self.lib.rrf_plan_create(ctypes.byref(h), self.code, int(m_max),
-                                      int(n_max), int(block_b_max), int(k_max),
-                                      _stream_handle(self.stream))
-        _abi.check(st, "rrf_plan_create", allow_warn=False)
+        if workspace is None:
+            st = self.lib.rrf_plan_create(ctypes.byref(h), self.code, int(m_max),
+                                          int(n_max), int(block_b_max), int(k_max),
+                                          _stream_handle(self.stream))
+            _abi.check(st, "rrf_plan_create", allow_warn=False)
+        else:
+            if not workspace.is_cuda or not workspace.is_contiguous():
+                raise ValueError("workspace must be a contiguous CUDA tensor")
+            st = self.lib.rrf_plan_create_in(
+                ctypes.byref(h), self.code, int(m_max), int(n_max), int(block_b_max),
+                int(k_max), _stream_handle(self.stream),
+                ctypes.c_void_p(workspace.data_ptr()),
+                workspace.numel() * workspace.element_size())
+            _abi.check(st, "rrf_plan_create_in", allow_warn=False)
+        self.workspace = workspace
         self.handle = h
         self.m_max, self.n_max, self.block_b_max, self.k_max = (
             m_max, n_max, block_b_max, k_max)
@@ -249,6 +264,16 @@ class Plan:
             ctypes.c_void_p(M.data_ptr()), ldm, m, n,
             ctypes.c_void_p(out.data_ptr()), max(r_new, 1)), "rrf_subspace_map")
         return out
+
+
+def workspace_size(dtype, m_max, n_max, block_b_max=64, k_max=0):
+    """Device bytes a plan with these maxima needs (rrf_workspace_size)."""
+    out = ctypes.c_size_t()
+    _abi.check(_abi.load().rrf_workspace_size(_dtype_code(dtype), int(m_max), int(n_max),
+                                              int(block_b_max), int(k_max),
+                                              ctypes.byref(out)),
+               "rrf_workspace_size")
+    return out.value
 
 
 def run(A, tol, block_b, seed, k_max=0, stop_mode=RRF_STOP_TRAILING, power=0):

@@ -35,6 +35,8 @@ _int = ctypes.c_int
 # name: (restype, argtypes)
 SIGNATURES = {
     "rrf_plan_create": (_int, [_pvp, _int, _i64, _i64, _i64, _i64, _vp]),
+    "rrf_plan_create_in": (_int, [_pvp, _int, _i64, _i64, _i64, _i64, _vp, _vp,
+                                  ctypes.c_size_t]),
     "rrf_run": (_int, [_vp, _vp, _i64, _i64, _i64, ctypes.c_double, _i64, _u64,
                        _pvp, _pi64, _pi64, _pvp, _pi64]),
     "rrf_destroy": (_int, [_vp]),

@@ -45,10 +45,16 @@ struct Sizes {
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
       rowj, st, trace, tsqr, gx, tx, Yest, spec, Tpow, Tp, pairs;
+  // Every buffer at a 256-byte boundary (a caller-provided workspace is
+  // carved in this order).
   size_t total() const {
-    return Bws + V + Tm + tau + Ypart + Ysum + Om + Zpart + W + Q + Q64 +
-           normpart + red + rowj + st + trace + tsqr + gx + tx + Yest + spec + Tpow +
-           Tp + pairs;
+    const size_t parts[] = {Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64,
+                            normpart, tsqr, red, rowj, gx, tx, st, trace / 3,
+                            trace / 3, trace / 3, Yest, spec, Tpow, Tp, pairs};
+    size_t t = 0;
+    for (size_t x : parts)
+      if (x) t += (std::max<size_t>(x, 256) + 255) / 256 * 256;
+    return t;
   }
 };
 
@@ -121,6 +127,8 @@ struct rrf_plan {
   Sizes sz;
   std::vector<void*> dev_allocs;
   void *Bws, *Ypart, *Om, *Zpart, *W, *Q, *Q64;
+  char* ws_base = nullptr;   // caller-provided device workspace, or null
+  size_t ws_bytes = 0, ws_used = 0;
   double* tsqr;              // scratch of the tall-skinny QR panel
   double* Tp;                // merged T of block pairs (explicit-Q pass)
   OrgqrPair* pairs_d;        // pair list, device
@@ -162,7 +170,16 @@ rrf_status hip_fail(hipError_t e) {
 }
 
 // RRF_FAULT_ALLOC=N makes the N-th device allocation of a plan fail (tests).
+// With a caller-provided workspace the buffers are carved from it instead
+// (256-byte boundaries, in the order of Sizes::total).
 hipError_t dev_alloc(rrf_plan* p, void** out, size_t bytes, int* counter) {
+  if (p->ws_base) {
+    const size_t b = (std::max<size_t>(bytes, 256) + 255) / 256 * 256;
+    if (p->ws_used + b > p->ws_bytes) return hipErrorOutOfMemory;
+    *out = p->ws_base + p->ws_used;
+    p->ws_used += b;
+    return hipSuccess;
+  }
   ++*counter;
   const char* f = std::getenv("RRF_FAULT_ALLOC");
   if (f && std::atoi(f) == *counter) return hipErrorOutOfMemory;
@@ -1159,16 +1176,24 @@ rrf_status rrf_workspace_size(rrf_dtype dtype, int64_t m_max, int64_t n_max,
   return RRF_OK;
 }
 
-rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
-                           int64_t n_max, int64_t block_b_max, int64_t k_max,
-                           void* hip_stream) {
+namespace {
+rrf_status plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max, int64_t n_max,
+                       int64_t block_b_max, int64_t k_max, void* hip_stream,
+                       void* workspace, size_t workspace_bytes) {
   if (!plan || !valid_dtype(dtype) || m_max < 1 || n_max < 1 ||
       block_b_max < 1 || block_b_max > kMaxBlockB || k_max < 0)
     return RRF_ERR_INVALID_ARG;
+  if (workspace) {
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0 ||
+        workspace_bytes < compute_sizes(dtype, m_max, n_max, block_b_max, k_max).total())
+      return RRF_ERR_INVALID_ARG;
+  }
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return RRF_ERR_HIP;
   rrf_plan* p = new (std::nothrow) rrf_plan();
   if (!p) return RRF_ERR_NOMEM;
+  p->ws_base = static_cast<char*>(workspace);
+  p->ws_bytes = workspace ? workspace_bytes : 0;
   p->dtype = dtype;
   p->elem = dtype == RRF_F32 ? 4 : 8;
   p->m_max = m_max;
@@ -1310,6 +1335,20 @@ rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
   p->E0 = p->sigma2 = 0.0;
   *plan = p;
   return RRF_OK;
+}
+}  // namespace
+
+rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
+                           int64_t n_max, int64_t block_b_max, int64_t k_max,
+                           void* hip_stream) {
+  return plan_create(plan, dtype, m_max, n_max, block_b_max, k_max, hip_stream, nullptr, 0);
+}
+
+rrf_status rrf_plan_create_in(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
+                              int64_t n_max, int64_t block_b_max, int64_t k_max,
+                              void* hip_stream, void* workspace, size_t workspace_bytes) {
+  return plan_create(plan, dtype, m_max, n_max, block_b_max, k_max, hip_stream, workspace,
+                     workspace_bytes);
 }
 
 rrf_status rrf_destroy(rrf_plan_t plan) {

@@ -115,3 +115,20 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_abi, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         _abi.load()
+
+
+def test_caller_workspace_checked_before_device():
+    # rrf_plan_create_in: a misaligned or short workspace is rejected on the
+    # host, before any device call (the pointer is never dereferenced).
+    lib = _abi.load()
+    h = ctypes.c_void_p()
+    need = ctypes.c_size_t()
+    assert lib.rrf_workspace_size(1, 300, 200, 16, 0, ctypes.byref(need)) == 0
+    args = (ctypes.byref(h), 1, 300, 200, 16, 0, None)
+    assert lib.rrf_plan_create_in(*args, ctypes.c_void_p(0x1000 + 8),
+                                  need.value) == _abi.RRF_ERR_INVALID_ARG
+    assert lib.rrf_plan_create_in(*args, ctypes.c_void_p(0x100000),
+                                  need.value - 1) == _abi.RRF_ERR_INVALID_ARG
+    assert lib.rrf_plan_create_in(None, 1, 300, 200, 16, 0, None,
+                                  ctypes.c_void_p(0x100000), need.value) == _abi.RRF_ERR_INVALID_ARG
+    assert h.value is None

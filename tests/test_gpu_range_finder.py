@@ -351,6 +351,49 @@ def test_nonfinite_input_is_an_error():
         assert e.value.status == -3
 
 
+def test_caller_provided_workspace():
+    # rrf_plan_create_in: every device buffer carved from a workspace the
+    # caller allocated (here a torch tensor); results bit-identical to a plan
+    # that allocates its own, Q and B inside the workspace, and two runs in a
+    # row reuse it.
+    w = W.scaled("galore_fp32_4096x4096", 1024, 768)
+    A = to_dev(W.build_matrix(w))
+    need = rrf.workspace_size(torch.float32, 1024, 768, 32)
+    ws = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
+    off = (-ws.data_ptr()) % 256
+    ws = ws[off:off + need]
+    with rrf.Plan(torch.float32, 1024, 768, 32) as p:
+        Q1, B1, k1 = p.run(A, w.tol, 32, w.sketch_seed)
+    with rrf.Plan(torch.float32, 1024, 768, 32, workspace=ws) as p:
+        Qr, _, _, Br, _, _ = p.run_raw(A, w.tol, 32, w.sketch_seed)
+        lo, hi = ws.data_ptr(), ws.data_ptr() + need
+        assert lo <= Qr < hi and lo <= Br < hi
+        Q2, B2, k2 = p.run(A, w.tol, 32, w.sketch_seed)
+        torch.cuda.synchronize()
+        assert k1 == k2
+        assert torch.equal(Q1, Q2) and torch.equal(B1, B2)
+    with pytest.raises(rrf.RRFError) as e:
+        rrf.Plan(torch.float32, 1024, 768, 32, workspace=ws[:need - 256])
+    assert e.value.status == -1
+
+
+@pytest.mark.parametrize("nth", [1, 13, 25, 26])
+def test_allocation_failure_is_reported(monkeypatch, nth):
+    # RRF_FAULT_ALLOC=N fails the plan's N-th allocation (25 device buffers
+    # for a binary64 plan, then the pinned run state): rrf_plan_create
+    # returns RRF_ERR_NOMEM, frees what it had, and a later plan works.
+    monkeypatch.setenv("RRF_FAULT_ALLOC", str(nth))
+    say(f"allocation failure {nth}")
+    with pytest.raises(rrf.RRFError) as e:
+        rrf.Plan(torch.float64, 500, 300, 16)
+    assert e.value.status == -4
+    monkeypatch.delenv("RRF_FAULT_ALLOC")
+    w = W.WORKLOADS["tiny_fp64_500x300"]
+    with rrf.Plan(torch.float64, 500, 300, 16) as p:
+        _, _, k = p.run(to_dev(W.build_matrix(w)), w.tol, 16, w.sketch_seed)
+    assert k == _oracle(w, W.build_matrix(w)).k
+
+
 def test_input_is_not_modified():
     w = W.scaled("square_fp64_16384", 512, 512)
     A = to_dev(W.build_matrix(w))
