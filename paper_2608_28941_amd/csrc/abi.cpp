@@ -1067,6 +1067,16 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   return RRF_OK;
 }
 
+// The bits of an enum argument as an int.  A C caller may pass any int for
+// an enum parameter; reading such a value as the C++ enum type is undefined
+// (outside its enumerators' range), so arguments are validated on their bits.
+template <typename E>
+int enum_bits(const E& e) {
+  static_assert(sizeof(E) == sizeof(int), "enum arguments are int-sized");
+  int v;
+  std::memcpy(&v, &e, sizeof v);
+  return v;
+}
 bool valid_dtype(int d) { return d == RRF_F32 || d == RRF_F64; }
 
 template <typename T>
@@ -1152,8 +1162,8 @@ rrf_status larfb_stage(rrf_plan* p, int trans, const T* V, int64_t ldv,
 
 extern "C" {
 
-const char* rrf_status_string(rrf_status s) {
-  switch (s) {
+const char* rrf_status_string(rrf_status status) {
+  switch (enum_bits(status)) {
     case RRF_OK: return "RRF_OK";
     case RRF_WARN_KMAX: return "RRF_WARN_KMAX: rank cap reached before the tolerance";
     case RRF_ERR_INVALID_ARG: return "RRF_ERR_INVALID_ARG: invalid argument";
@@ -1169,7 +1179,7 @@ const char* rrf_status_string(rrf_status s) {
 rrf_status rrf_workspace_size(rrf_dtype dtype, int64_t m_max, int64_t n_max,
                               int64_t block_b_max, int64_t k_max,
                               size_t* bytes) {
-  if (!bytes || !valid_dtype(dtype) || m_max < 1 || n_max < 1 ||
+  if (!bytes || !valid_dtype(enum_bits(dtype)) || m_max < 1 || n_max < 1 ||
       block_b_max < 1 || block_b_max > kMaxBlockB || k_max < 0)
     return RRF_ERR_INVALID_ARG;
   *bytes = compute_sizes(dtype, m_max, n_max, block_b_max, k_max).total();
@@ -1177,12 +1187,13 @@ rrf_status rrf_workspace_size(rrf_dtype dtype, int64_t m_max, int64_t n_max,
 }
 
 namespace {
-rrf_status plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max, int64_t n_max,
+rrf_status plan_create(rrf_plan_t* plan, int dtype_bits, int64_t m_max, int64_t n_max,
                        int64_t block_b_max, int64_t k_max, void* hip_stream,
                        void* workspace, size_t workspace_bytes) {
-  if (!plan || !valid_dtype(dtype) || m_max < 1 || n_max < 1 ||
+  if (!plan || !valid_dtype(dtype_bits) || m_max < 1 || n_max < 1 ||
       block_b_max < 1 || block_b_max > kMaxBlockB || k_max < 0)
     return RRF_ERR_INVALID_ARG;
+  const rrf_dtype dtype = (rrf_dtype)dtype_bits;
   if (workspace) {
     if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0 ||
         workspace_bytes < compute_sizes(dtype, m_max, n_max, block_b_max, k_max).total())
@@ -1341,14 +1352,15 @@ rrf_status plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max, int64_t
 rrf_status rrf_plan_create(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
                            int64_t n_max, int64_t block_b_max, int64_t k_max,
                            void* hip_stream) {
-  return plan_create(plan, dtype, m_max, n_max, block_b_max, k_max, hip_stream, nullptr, 0);
+  return plan_create(plan, enum_bits(dtype), m_max, n_max, block_b_max, k_max, hip_stream,
+                     nullptr, 0);
 }
 
 rrf_status rrf_plan_create_in(rrf_plan_t* plan, rrf_dtype dtype, int64_t m_max,
                               int64_t n_max, int64_t block_b_max, int64_t k_max,
                               void* hip_stream, void* workspace, size_t workspace_bytes) {
-  return plan_create(plan, dtype, m_max, n_max, block_b_max, k_max, hip_stream, workspace,
-                     workspace_bytes);
+  return plan_create(plan, enum_bits(dtype), m_max, n_max, block_b_max, k_max, hip_stream,
+                     workspace, workspace_bytes);
 }
 
 rrf_status rrf_destroy(rrf_plan_t plan) {
@@ -1359,8 +1371,8 @@ rrf_status rrf_destroy(rrf_plan_t plan) {
 }
 
 rrf_status rrf_set_stop_mode(rrf_plan_t plan, rrf_stop_mode mode) {
-  if (!plan || (mode != RRF_STOP_TRAILING && mode != RRF_STOP_SUBTRACT &&
-                mode != RRF_STOP_SPECTRAL))
+  const int md = enum_bits(mode);
+  if (!plan || (md != RRF_STOP_TRAILING && md != RRF_STOP_SUBTRACT && md != RRF_STOP_SPECTRAL))
     return RRF_ERR_INVALID_ARG;
   plan->stop_mode = mode;
   return RRF_OK;
@@ -1482,7 +1494,7 @@ rrf_status rrf_get_reflectors(rrf_plan_t plan, const void** V, int64_t* ldv,
 
 rrf_status rrf_sketch(rrf_dtype dtype, uint64_t seed, int64_t n, int64_t col0,
                       int64_t ncols, void* out, int64_t ldo, void* hip_stream) {
-  if (!valid_dtype(dtype) || !out || n < 0 || col0 < 0 || ncols < 0 ||
+  if (!valid_dtype(enum_bits(dtype)) || !out || n < 0 || col0 < 0 || ncols < 0 ||
       ldo < std::max<int64_t>(1, n))
     return RRF_ERR_INVALID_ARG;
   if (n == 0 || ncols == 0) return RRF_OK;
@@ -1589,7 +1601,7 @@ rrf_status rrf_subspace_map(rrf_plan_t plan, const void* Qnew, int64_t ldqn,
 rrf_status rrf_copy_matrix(rrf_dtype dtype, const void* src, int64_t lds,
                            void* dst, int64_t ldd, int64_t rows, int64_t cols,
                            void* hip_stream) {
-  if (!valid_dtype(dtype) || !src || !dst || rows < 0 || cols < 0 ||
+  if (!valid_dtype(enum_bits(dtype)) || !src || !dst || rows < 0 || cols < 0 ||
       lds < std::max<int64_t>(1, rows) || ldd < std::max<int64_t>(1, rows))
     return RRF_ERR_INVALID_ARG;
   hipError_t e;

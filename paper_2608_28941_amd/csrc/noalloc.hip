@@ -17,6 +17,8 @@
 #include <mutex>
 #include <type_traits>
 
+#include <cstring>
+
 #include "rrf_internal.h"
 
 namespace rrf {
@@ -144,7 +146,11 @@ extern "C" rrf_status rrf_panel_qr_noalloc(rrf_dtype dtype, const void* Y, int64
                                            int64_t b, int64_t ldy, void* V, int64_t ldv,
                                            void* T, int64_t ldt, void* tau, int* wait_status,
                                            void* hip_stream) {
-  if ((dtype != RRF_F32 && dtype != RRF_F64) || !Y || !V || !T || !tau)
+  // dtype validated on its bits (a C caller may pass any int).
+  int dt;
+  static_assert(sizeof(dtype) == sizeof(int), "int-sized enum");
+  std::memcpy(&dt, &dtype, sizeof dt);
+  if ((dt != RRF_F32 && dt != RRF_F64) || !Y || !V || !T || !tau)
     return RRF_ERR_INVALID_ARG;
   if (b < 1 || b > kMaxBlock || m < b || ldy < m || ldv < m || ldt < b)
     return RRF_ERR_INVALID_ARG;
