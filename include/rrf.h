@@ -20,13 +20,26 @@
  *     the call or plan: float for RRF_F32, double for RRF_F64.
  *   - Arguments are checked on the host before any device call; an invalid
  *     argument returns RRF_ERR_INVALID_ARG and leaves every output untouched.
- *     No entry point prints or aborts.
+ *     No entry point prints or aborts (unless RRF_LOG=1, below).
  *   - A plan is not thread-safe: one plan per host thread / stream.
  *   - Work is enqueued on the plan's HIP stream (or the given stream).
  *     rrf_run synchronises that stream before it returns (k is an output
  *     shape); so do rrf_panel_qr and the one-launch form of
  *     rrf_apply_block_reflector (they read back whether a grid-wide wait
  *     gave up); the other entry points do not.
+ *
+ * Environment (read when a plan is created):
+ *   RRF_LOG=1          rrf_run writes one line per run (sizes, k, blocks,
+ *                      ||A||_F^2, sigma^2) and one per block (the stopping
+ *                      quantities) to stderr.
+ *   RRF_STOP_MODE      trailing | subtract | spectral: the initial stop mode
+ *                      (rrf_set_stop_mode changes it).
+ *   RRF_LOOKAHEAD=0    no look-ahead (every panel after its sample's update).
+ *   RRF_PANEL          grid | gram | tsqr: force one panel algorithm.
+ *   RRF_SUBBLOCK       16 | 32 | 64: widest sub-block.
+ *   RRF_PANEL_WGS, RRF_LA_GRAM_WGS  panel grid sizes (tuning).
+ *   RRF_FAULT_ALLOC=N, RRF_TEST_SPIN_LIMIT=N  test hooks: fail the plan's
+ *                      N-th allocation; poll rounds of every grid-wide wait.
  */
 #ifndef RRF_H
 #define RRF_H

@@ -21,6 +21,7 @@
 #include <cmath>
 #include <type_traits>
 #include <cstdlib>
+#include <cstdio>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -142,6 +143,7 @@ struct rrf_plan {
   DevState* st;
   DevState* st_host;
   int stop_mode, timing, panel_target;
+  int log;                   // RRF_LOG=1: one stderr line per run, one per block
   int gram_fused_max;         // most workgroups of a Gram panel inside the update's launch
   int sub_max;                // widest sub-block (16, 32 or 64 columns; 0: by size)
   unsigned spin_limit;       // poll rounds of a grid-wide wait (run state)
@@ -1213,6 +1215,15 @@ rrf_status plan_create(rrf_plan_t* plan, int dtype_bits, int64_t m_max, int64_t 
   p->k_max = k_max;
   p->stream = (hipStream_t)hip_stream;
   p->stop_mode = RRF_STOP_TRAILING;
+  // RRF_STOP_MODE (trailing, subtract or spectral) sets the initial stopping
+  // quantity; rrf_set_stop_mode changes it.  RRF_LOG=1 logs every run to
+  // stderr; the library prints nothing otherwise.
+  if (const char* sm = std::getenv("RRF_STOP_MODE")) {
+    if (std::strcmp(sm, "subtract") == 0) p->stop_mode = RRF_STOP_SUBTRACT;
+    else if (std::strcmp(sm, "spectral") == 0) p->stop_mode = RRF_STOP_SPECTRAL;
+  }
+  p->log = 0;
+  if (const char* lg = std::getenv("RRF_LOG")) p->log = std::atoi(lg) != 0;
   p->power = 0;
   p->timing = 0;
   p->panel_target = 64;
@@ -1422,11 +1433,26 @@ rrf_status rrf_run(rrf_plan_t plan, const void* A, int64_t m, int64_t n,
       (void)hipStreamSynchronize(plan->stream);
       plan->nblocks = 0;
       *k = 0;
+      if (plan->log)
+        std::fprintf(stderr, "rrf_run: m=%lld n=%lld b=%lld tol=%g: %s\n", (long long)m,
+                     (long long)n, (long long)block_b, tol, rrf_status_string(st));
       return st;
     }
     stats_collect(plan);
   }
   plan->last_k = kk;
+  if (plan->log) {
+    std::fprintf(stderr,
+                 "rrf_run: m=%lld n=%lld b=%lld tol=%g mode=%d -> k=%lld blocks=%lld "
+                 "||A||_F^2=%.6e sigma^2=%.6e%s\n",
+                 (long long)m, (long long)n, (long long)block_b, tol, plan->stop_mode,
+                 (long long)kk, (long long)plan->nblocks, plan->E0, plan->sigma2,
+                 warn ? " (rank cap)" : "");
+    for (int64_t i = 0; i < plan->nblocks; ++i)
+      std::fprintf(stderr, "rrf_run:   block %lld: E_trail=%.6e E_sub=%.6e E_spec=%.6e\n",
+                   (long long)i, plan->trace_trail[i], plan->trace_sub[i],
+                   plan->trace_spec[i]);
+  }
   *Q = plan->Q;
   *ldq = plan->sz.ldb;
   *B = plan->Bws;

@@ -452,3 +452,20 @@ def test_full_size_config_against_stored_oracle(name):
     low = torch.tril(R, -1).abs().max().item()
     assert low <= 1e3 * np.finfo(dt).eps * R.abs().max().item()
     assert tr["nblocks"] == g["blocks"]
+
+
+def test_log_and_stop_mode_environment(monkeypatch, capfd):
+    # RRF_LOG=1: one stderr line per run and one per block; RRF_STOP_MODE
+    # selects the initial stop mode (subtract here, same k as the oracle's).
+    monkeypatch.setenv("RRF_LOG", "1")
+    monkeypatch.setenv("RRF_STOP_MODE", "subtract")
+    w = W.scaled("square_fp64_16384", 1024, 800, block_b=32, tol=1e-4)
+    A = W.build_matrix(w)
+    ref = oracle.hbarrf(A, w.tol, w.block_b, w.sketch_seed, stop="subtract")
+    with rrf.Plan(torch.float64, 1024, 800, 32) as p:
+        _, _, k = p.run(to_dev(A), w.tol, 32, w.sketch_seed)
+        tr = p.trace()
+    assert k == ref.k
+    err = capfd.readouterr().err
+    assert f"-> k={k} blocks={tr['nblocks']}" in err and "mode=1" in err
+    assert err.count("rrf_run:   block") == tr["nblocks"]
