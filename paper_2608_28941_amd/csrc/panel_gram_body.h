@@ -333,13 +333,11 @@ __device__ __forceinline__ void panel_gram_body(const GramPanelArgs& ga, const i
   form_gram(0, true);
   after_form(0);
   int j = 0;
-  while (j < b) {
+  // Column steps in an inner loop of their own; a cancelled pivot norm leaves
+  // it to form F again (the formation code stays out of the step loop).
+  for (;;) {
+  while (j < b && s_flag == 0.0) {
     const int p = j & 1;
-    if (s_flag != 0.0) {
-      form_gram(j, false);
-      after_form(j);
-      continue;
-    }
     const double tau_j = s_tau, scale = s_scale;
     // The next pivot before this step: F[j+1][j+1] and top[j+1][j+1] (row
     // j + 1 is not written before the barrier below).
@@ -438,6 +436,10 @@ __device__ __forceinline__ void panel_gram_body(const GramPanelArgs& ga, const i
     if (j + 1 < b) export_step(j + 1, p ^ 1);
     __syncthreads();
     ++j;
+  }
+  if (j >= b) break;
+  form_gram(j, false);
+  after_form(j);
   }
 
   // The top block holds rows 0 .. b-1 of V below the diagonal and v_p^T v_c
