@@ -414,7 +414,7 @@ rrf_status apply_wy(rrf_plan* p, int trans, const double* V, int64_t ldv,
     const int64_t row_wgs = std::max<int64_t>(ceil_div(mr, kUpdRows), 1);
     int64_t su0 = ceil_div(4 * (int64_t)p->num_cus, row_wgs);
     su0 = std::max<int64_t>(1, std::min<int64_t>({su0, ncols / 32, 64}));
-    ua.cols_per_split = round_up(ceil_div(ncols, su0), kUpdChunk);
+    ua.cols_per_split = round_up(ceil_div(ncols, su0), 2 * kUpdChunk);
   }
   const int su = (int)ceil_div(ncols, ua.cols_per_split);
   RRF_LAUNCH(p, stage, fl, 2.0 * e * mr * ncols, launch_update<T>(ua, su, p->stream));
@@ -514,7 +514,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   u.split_stride = ldb * 64; u.s0 = 0; u.normpart = p->normpart;
   {
     const int su0 = upd_splits(m, n, p->num_cus);
-    u.cols_per_split = round_up(ceil_div(n, su0), kUpdChunk);
+    u.cols_per_split = round_up(ceil_div(n, su0), 2 * kUpdChunk);
   }
   int ysplits = (int)ceil_div(n, u.cols_per_split);
   RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 2.0 * m * n * b0, e * (m * n + m * b0),
@@ -627,7 +627,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       us.V = nullptr; us.ldv = 0; us.bp = 0; us.W = nullptr; us.ldw = 0;
       us.Om = (T*)p->W; us.ldo = bpp; us.qp = bpp; us.P = Yp; us.ldp = ldb;
       us.split_stride = ldb * 64; us.s0 = 0; us.normpart = nullptr;
-      us.cols_per_split = round_up(ceil_div(n, upd_splits(mpp, n, p->num_cus)), kUpdChunk);
+      us.cols_per_split = round_up(ceil_div(n, upd_splits(mpp, n, p->num_cus)), 2 * kUpdChunk);
       const int sus = (int)ceil_div(n, us.cols_per_split);
       const double uby = e * (mpp * n + mpp * bb);
       RRF_LAUNCH(p, RRF_STAGE_SAMPLE, fl, uby, launch_update<T>(us, sus, s));
@@ -711,7 +711,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
         u1.qp = 64;
         u1.normpart = nullptr;
         const int su1 = upd_splits_fused(m, n, (int64_t)occ0 * p->num_cus - sh.G);
-        u1.cols_per_split = round_up(ceil_div(n, su1), kUpdChunk);
+        u1.cols_per_split = round_up(ceil_div(n, su1), 2 * kUpdChunk);
         const int ys1 = (int)ceil_div(n, u1.cols_per_split);
         pa.epoch_base = next_epoch(p);
         const double sfl = 2.0 * m * n * b_next, sby = e * (m * n + m * b_next);
@@ -822,7 +822,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       if (occ > 0)
         su0 = upd_splits_fused(mp, n, (int64_t)occ * p->num_cus - pan_shape.G);
     }
-    ua.cols_per_split = round_up(ceil_div(n, su0), kUpdChunk);
+    ua.cols_per_split = round_up(ceil_div(n, su0), 2 * kUpdChunk);
     const int su = (int)ceil_div(n, ua.cols_per_split);
     const double smp_flops = 2.0 * (mp - bi) * n * b_s;
     const double upd_flops = 2.0 * mp * n * bi + smp_flops;

@@ -24,6 +24,9 @@ namespace {
 // host keeps kUpdChunk * ld * sizeof(T) <= 2^30.
 // ---------------------------------------------------------------------------
 constexpr unsigned kOOB = 1u << 30;   // lane offset of a masked row
+// s_waitcnt operand (gfx9 encoding) that waits for vmcnt 0 and leaves
+// expcnt (7) and lgkmcnt (15) at their maximum.
+constexpr int kVmcntZero = 0x0F70;
 
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
@@ -144,11 +147,18 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
   const unsigned tstep_d = (unsigned)(16 * a.ldd * E);
 
   // Staging values (W, Omega) and the B tiles of the next chunk are loaded
-  // while the current chunk computes; the last chunk prefetches itself again
-  // (harmless, and it keeps the loads unconditional).  Chunks start at
-  // multiples of kUpdChunk and split boundaries are multiples of kUpdChunk, so
-  // a chunk only runs past ce at the end of the matrix, where W and Omega
-  // carry zero rows up to the next multiple and the B loads return zero.
+  // while the current chunk computes.  Chunks start at multiples of kUpdChunk
+  // and split boundaries are multiples of kUpdChunk, so a chunk that starts
+  // before ce only runs past it at the end of the matrix, where W and Omega
+  // carry zero rows up to the next multiple and the B loads return zero.  A
+  // chunk that starts at or past ce (the prefetch after the last chunk, and
+  // the second chunk of the last pair when the count is odd) gets buffer
+  // resources of zero bytes: its loads return zero without touching memory
+  // and its stores are dropped, so it adds nothing to P or the norms.  The
+  // chunk loop therefore always runs whole pairs, with no branch between the
+  // two chunks of a pair: a conditional second chunk gave the loop header two
+  // predecessors, and the waits merged there covered the stores of the
+  // previous chunk.
   //
   // Schedule per chunk: issue the next chunk's loads, compute and store this
   // chunk, then move the next chunk's staging values into the other LDS
@@ -170,23 +180,23 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
   const int oo_pass = QP > 0 ? (256 / (QP > 0 ? QP : 1)) * a.ldo * E : 0;
   T tw[NW > 0 ? NW : 1], to[NO > 0 ? NO : 1];
   acc_t bx[RT][NCT];
-  const int64_t c_last = cs + (ce - cs - 1) / kUpdChunk * kUpdChunk;
   auto load_chunk = [&](int64_t cc0) {
+    const bool live = cc0 < ce;
     if (NW > 0) {
       const __amdgpu_buffer_rsrc_t rw =
-          buf_rsrc(a.W + cc0 * a.ldw, (int64_t)kUpdChunk * a.ldw * E);
+          buf_rsrc(a.W + cc0 * a.ldw, live ? (int64_t)kUpdChunk * a.ldw * E : 0);
 #pragma unroll
       for (int it = 0; it < NW; ++it) tw[it] = Buf<T>::ld_s(rw, wo_lane, it * wo_pass);
     }
     if (NO > 0) {
       const __amdgpu_buffer_rsrc_t ro =
-          buf_rsrc(a.Om + cc0 * a.ldo, (int64_t)kUpdChunk * a.ldo * E);
+          buf_rsrc(a.Om + cc0 * a.ldo, live ? (int64_t)kUpdChunk * a.ldo * E : 0);
 #pragma unroll
       for (int it = 0; it < NO; ++it) to[it] = Buf<T>::ld_s(ro, oo_lane, it * oo_pass);
     }
-    const int64_t cn = min((int64_t)kUpdChunk, a.n - cc0);
+    const int64_t cn = min((int64_t)kUpdChunk, ce - cc0);
     const __amdgpu_buffer_rsrc_t rs =
-        buf_rsrc(a.src + cc0 * a.lds, ((cn - 1) * a.lds + a.mr) * E);
+        buf_rsrc(a.src + cc0 * a.lds, cn > 0 ? ((cn - 1) * a.lds + a.mr) * E : 0);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -216,6 +226,13 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct) t[rt][ct] = bx[rt][ct];
   __syncthreads();
+  // Every load of the first chunk has arrived before the loop (vmcnt(0)).
+  // In steady state a chunk starts with the B tiles in flight ahead of the
+  // previous chunk's stores; if the loop were entered with them in flight
+  // too but no stores after them, the waits merged at the loop entry would
+  // count the stores and hold the first MFMAs of every chunk until they
+  // complete.
+  __builtin_amdgcn_s_waitcnt(kVmcntZero);
 
   // One chunk from buffer CUR (a compile-time constant: the loop below is
   // unrolled by two so that both buffers have fixed LDS offsets).
@@ -223,7 +240,10 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
     constexpr int CUR = decltype(cur_tag)::value;
     const T* wlc = wl[CUR];
     const T* olc = ol[CUR];
-    load_chunk(min(c0 + kUpdChunk, c_last));
+    load_chunk(c0 + kUpdChunk);
+    // Keep the prefetch at the top of the chunk: under full register use the
+    // scheduler otherwise sinks the B loads into the middle of the chunk.
+    __builtin_amdgcn_sched_barrier(0);
 
     // Rank-b update of all tiles first, so that the samples do not wait on
     // the result of the MFMA chain that just produced their operand.
@@ -238,9 +258,9 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
           t[rt][ct] = Mfma<T>::op(wa, vreg[rt][p4], t[rt][ct]);
       }
     if (STORE) {
-      const int64_t cn = min((int64_t)kUpdChunk, a.n - c0);
+      const int64_t cn = min((int64_t)kUpdChunk, ce - c0);
       const __amdgpu_buffer_rsrc_t rd =
-          buf_rsrc(a.dst + c0 * a.ldd, ((cn - 1) * a.ldd + a.mr) * E);
+          buf_rsrc(a.dst + c0 * a.ldd, cn > 0 ? ((cn - 1) * a.ldd + a.mr) * E : 0);
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -279,7 +299,7 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
   };
   for (int64_t c0 = cs; c0 < ce; c0 += 2 * kUpdChunk) {
     chunk(c0, std::integral_constant<int, 0>());
-    if (c0 + kUpdChunk < ce) chunk(c0 + kUpdChunk, std::integral_constant<int, 1>());
+    chunk(c0 + kUpdChunk, std::integral_constant<int, 1>());
   }
 
   if (QP > 0) {
