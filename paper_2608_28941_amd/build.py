@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librrf.so")
 
-SOURCES = ["sketch.hip", "panel.hip", "panel_gram.hip", "tsqr.hip", "thin_apply.hip", "wy.hip", "lookahead.hip", "aux.hip", "spectral.hip", "map.hip", "noalloc.hip", "orgqr_pairs.hip", "abi.cpp"]
+SOURCES = ["sketch.hip", "panel.hip", "panel_gram.hip", "tsqr.hip", "thin_apply.hip", "wy.hip", "lookahead.hip", "aux.hip", "spectral.hip", "map.hip", "noalloc.hip", "orgqr_groups.hip", "abi.cpp"]
 COMMON = [
     "-x", "hip", "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",
     "-Wall", "-Wno-unused-function",

@@ -45,13 +45,13 @@ struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
   size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
-      rowj, st, trace, tsqr, gx, tx, Yest, spec, Tpow, Tp, pairs;
+      rowj, st, trace, tsqr, gx, tx, Yest, spec, Tpow, Tp, groups;
   // Every buffer at a 256-byte boundary (a caller-provided workspace is
   // carved in this order).
   size_t total() const {
     const size_t parts[] = {Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64,
                             normpart, tsqr, red, rowj, gx, tx, st, trace / 3,
-                            trace / 3, trace / 3, Yest, spec, Tpow, Tp, pairs};
+                            trace / 3, trace / 3, Yest, spec, Tpow, Tp, groups};
     size_t t = 0;
     for (size_t x : parts)
       if (x) t += (std::max<size_t>(x, 256) + 255) / 256 * 256;
@@ -78,7 +78,9 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   // Omega and W carry zero rows up to the next multiple of the update chunk.
   z.Om = (size_t)(n_max + kUpdChunk) * kOmLd * e;
   z.Zpart = (size_t)kMaxRedSplits * n_max * 64 * 8;
-  z.W = (size_t)(n_max + kUpdChunk) * 64 * 8;
+  // W rows of up to 128 reflectors (the explicit-Q pass applies groups of
+  // blocks as one); the bulk update uses 64.
+  z.W = (size_t)(n_max + kUpdChunk) * kGroupMax * 8;
   z.Q = (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * e;
   z.Q64 = dt == RRF_F32 ? (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * 8 : 0;
   z.normpart = (size_t)(ceil_div(m_max, kUpdRows) * kMaxUpdSplits + 1) * 2 * 8;
@@ -94,10 +96,10 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.Yest = (size_t)z.ldysum * 64 * 8;
   z.spec = (size_t)kMaxSpecWGs * 4096 * 8;
   z.Tpow = (size_t)64 * 64 * 8;
-  // Explicit-Q pass: merged T of block pairs (laid out like T) and the pair
-  // list (pairs of blocks of at least 16 columns).
-  z.Tp = z.Tm;
-  z.pairs = (size_t)(z.kcols / 32 + 2) * sizeof(OrgqrPair);
+  // Explicit-Q pass: merged T of block groups (kGroupMax rows per column)
+  // and the group list (blocks of at least one column each).
+  z.Tp = (size_t)kGroupMax * z.kcols * 8;
+  z.groups = (size_t)(z.kcols + 2) * sizeof(OrgqrGroup);
   // Tall-skinny QR panel: the largest tree over the block widths the plan
   // allows (the tree shrinks with the panel's rows).
   z.tsqr = 8;
@@ -131,9 +133,9 @@ struct rrf_plan {
   char* ws_base = nullptr;   // caller-provided device workspace, or null
   size_t ws_bytes = 0, ws_used = 0;
   double* tsqr;              // scratch of the tall-skinny QR panel
-  double* Tp;                // merged T of block pairs (explicit-Q pass)
-  OrgqrPair* pairs_d;        // pair list, device
-  OrgqrPair* pairs_h;        // pair list, pinned host staging
+  double* Tp;                // merged T of block groups (explicit-Q pass)
+  OrgqrGroup* groups_d;      // group list, device
+  OrgqrGroup* groups_h;      // group list, pinned host staging
   int panel_mode;            // kPanelGrid, kPanelTsqr, kPanelGram or kPanelAuto
   double *V, *Tm, *tau, *Ysum;
   double *normpart, *trace_trail_d, *trace_sub_d, *trace_spec_d;
@@ -195,7 +197,7 @@ void free_plan(rrf_plan* p) {
   for (void* q : p->dev_allocs) (void)hipFree(q);
   p->dev_allocs.clear();
   if (p->st_host) (void)hipHostFree(p->st_host);
-  if (p->pairs_h) (void)hipHostFree(p->pairs_h);
+  if (p->groups_h) (void)hipHostFree(p->groups_h);
   for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
   if (p->state_ev) (void)hipEventDestroy(p->state_ev);
   if (p->map_c) (void)hipFree(p->map_c);
@@ -241,14 +243,22 @@ int red_splits(int64_t mr, int64_t n, int num_cus) {
 
 // Row splits of a reduce over few columns (the explicit-Q pass, a general
 // block reflector), where 32 splits leave each workgroup streaming hundreds
-// of rows on its own: up to 64 splits of at least 128 rows, two workgroups
-// per compute unit, within the partial buffer (max_splits); never fewer than
-// the wide-matrix choice.
-int red_splits_narrow(int64_t mr, int64_t n, int num_cus, int64_t max_splits) {
-  const int64_t col_wgs = ceil_div(n, kRedCols);
+// of rows on its own: up to 128 splits of at least kNarrowRows rows, two
+// workgroups per compute unit, within the partial buffer (max_splits); never
+// fewer than the wide-matrix choice.  Each split's rows are a chain of
+// dependent chunks, so short splits keep a narrow reduce off the latency of
+// that chain.
+constexpr int kNarrowRows = 32;
+int red_splits_narrow(int64_t mr, int64_t n, int bp, int num_cus, int64_t max_splits) {
+  const int64_t col_wgs = ceil_div(n, red_cols(bp));
   int64_t s = ceil_div(2 * (int64_t)num_cus, std::max<int64_t>(col_wgs, 1));
-  s = std::min<int64_t>({s, 64, max_splits, std::max<int64_t>(1, mr / 128)});
-  return (int)std::max<int64_t>(s, red_splits(mr, n, num_cus));
+  s = std::min<int64_t>({s, 128, max_splits, std::max<int64_t>(1, mr / kNarrowRows)});
+  // At 128 reflectors two workgroups per compute unit are the whole target:
+  // more splits only add partial sums for formW to read.
+  if (bp < 128) s = std::max<int64_t>(s, red_splits(mr, n, num_cus));
+  // The wide-matrix choice assumes 64 reflectors; the buffer bound holds for
+  // any width.
+  return (int)std::max<int64_t>(1, std::min<int64_t>(s, max_splits));
 }
 
 // ---- timing / statistics --------------------------------------------------
@@ -384,14 +394,19 @@ rrf_status apply_wy(rrf_plan* p, int trans, const double* V, int64_t ldv,
   if (!Zs) Zs = (T*)p->Zpart;
   if (!Ws) Ws = (T*)p->W;
   const double e = (double)sizeof(T);
-  const int sr0 = red_splits_narrow(mr, ncols, p->num_cus,
-                                    (int64_t)kMaxRedSplits * p->n_max / ncols);
+  const int sr0 = red_splits_narrow(mr, ncols, bp, p->num_cus,
+                                    (int64_t)(p->sz.Zpart / 8) / (ncols * bp));
   ReduceArgs<T> ra{};
   ra.X = X; ra.ldx = ldx; ra.mr = mr; ra.n = ncols;
   ra.V = V; ra.ldv = ldv; ra.bp = bp;
   ra.Z = Zs; ra.split_stride = ncols * bp;
-  ra.rows_per_split = round_up(ceil_div(mr, sr0), kRedChunk);
+  ra.rows_per_split = round_up(ceil_div(mr, sr0), kNarrowRows);
   const int sr = (int)ceil_div(mr, ra.rows_per_split);
+  // The split partials (sr x ncols x bp) and W (ncols rows of bp, padded to
+  // the update chunk) must fit their buffers.
+  if ((size_t)sr * ncols * bp * sizeof(T) > p->sz.Zpart ||
+      (size_t)round_up(ncols, kUpdChunk) * bp * sizeof(T) > p->sz.W)
+    return RRF_ERR_INTERNAL;
   const double fl = 2.0 * mr * ncols * b;
   RRF_LAUNCH(p, stage == RRF_STAGE_UPDATE ? RRF_STAGE_REDUCE : stage, fl,
              e * mr * ncols, launch_reduce<T>(ra, sr, p->stream));
@@ -958,55 +973,97 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   p->nblocks = blk;
 
   // Explicit Q = H_0 ... H_{k-1} [I_k; 0], backward over the sub-blocks, in
-  // binary64 (float plans round the result once).  Adjacent sub-blocks of
-  // 16 to 32 columns are applied in pairs, as one block of up to 64
-  // reflectors with their merged T (orgqr_pairs.hip): half the passes over Q
-  // for 32-column blocks.
+  // binary64 (float plans round the result once).  Adjacent sub-blocks are
+  // applied in groups of up to kGroupMax reflectors, as one block with their
+  // merged T (orgqr_groups.hip): a quarter of the passes over Q for 32-column
+  // blocks, half for 64-column blocks.
   const int nsub = (int)p->sub_start.size();
   if (k > 0) {
     double* Qd = std::is_same<T, double>::value ? (double*)Q : (double*)p->Q64;
     RRF_LAUNCH(p, RRF_STAGE_ORGQR, 0.0, 8.0 * m * k,
                launch_fill_identity<double>(Qd, ldb, m, k, s));
-    struct Group { int64_t k0, b; int pair; };   // pair: index into the pair list, or -1
-    std::vector<Group> groups;
-    int npairs = 0;
+    // gi: index into the group list (merged T in Tp), or -1 (one block, its
+    // own T).
+    struct Pass { int64_t k0, b; int gi; };
+    std::vector<Pass> passes;
+    int ngroups = 0;
+    int64_t gram_rows = 0;
     auto width = [&](int i) { return (i + 1 < nsub ? p->sub_start[i + 1] : k) - p->sub_start[i]; };
     for (int i = nsub - 1; i >= 0;) {
-      const int64_t bi = width(i);
-      const int64_t bl = i >= 1 ? width(i - 1) : 0;
-      if (i >= 1 && bi >= 16 && bi <= 32 && bl >= 16 && bl <= 32 &&
-          (size_t)(npairs + 1) * sizeof(OrgqrPair) <= p->sz.pairs) {
-        p->pairs_h[npairs] = OrgqrPair{p->sub_start[i - 1], (int)bl, (int)bi};
-        groups.push_back(Group{p->sub_start[i - 1], bl + bi, npairs});
-        ++npairs;
-        i -= 2;
+      int j = i;
+      int64_t w = width(i);
+      while (j >= 1 && i - j + 1 < kMaxGroupBlocks && w + width(j - 1) <= kGroupMax) {
+        w += width(j - 1);
+        --j;
+      }
+      if (j < i && (size_t)(ngroups + 1) * sizeof(OrgqrGroup) <= p->sz.groups) {
+        OrgqrGroup g{};
+        g.k0 = p->sub_start[j];
+        g.nb = i - j + 1;
+        g.w = (int)w;
+        for (int c = 0; c < g.nb; ++c) g.off[c] = (int)(p->sub_start[j + c] - g.k0);
+        g.off[g.nb] = g.w;
+        // Gram tiles with an entry (i, j), block(i) < block(j): blocks are
+        // contiguous, so compare the tile's first row and its last column.
+        auto blk = [&](int col) {
+          int c = 0;
+          while (c + 1 < g.nb && col >= g.off[c + 1]) ++c;
+          return c;
+        };
+        g.ntiles = 0;
+        for (int ti = 0; 16 * ti < g.w; ++ti)
+          for (int tj = 0; 16 * tj < g.w; ++tj)
+            if (blk(16 * ti) < blk(std::min(16 * tj + 15, g.w - 1)))
+              g.tile[g.ntiles++] = (unsigned char)(8 * ti + tj);
+        p->groups_h[ngroups] = g;
+        passes.push_back(Pass{g.k0, w, ngroups});
+        gram_rows = std::max<int64_t>(gram_rows, m - g.k0);
+        ++ngroups;
+        i = j - 1;
       } else {
-        groups.push_back(Group{p->sub_start[i], bi, -1});
+        passes.push_back(Pass{p->sub_start[i], width(i), -1});
         i -= 1;
       }
     }
-    if (npairs > 0) {
-      he = hipMemcpyAsync(p->pairs_d, p->pairs_h, npairs * sizeof(OrgqrPair),
-                          hipMemcpyHostToDevice, s);
-      if (he != hipSuccess) return hip_fail(he);
-      PairArgs pa{};
-      pa.pairs = p->pairs_d; pa.V = V; pa.ldv = ldb; pa.m = m;
-      pa.Tm = Tm; pa.ldt = kTLd; pa.Tp = p->Tp; pa.part = (double*)p->Zpart;
-      // Row splits of the V_1^T V_2 sums: about 512 rows each (tall panels
-      // need many workgroups per pair), within the partial buffer.
-      const int64_t cap = (int64_t)(p->sz.Zpart / 8) / (1024 * (int64_t)npairs);
-      pa.nsplit = (int)std::max<int64_t>(1, std::min<int64_t>({ceil_div(m, 512), 256, cap}));
-      RRF_LAUNCH(p, RRF_STAGE_ORGQR, 2.0 * m * 32 * 32 * npairs, 8.0 * m * 64 * npairs,
-                 launch_orgqr_pairs(pa, npairs, s));
+    if (ngroups > 0) {
+      // Row splits of the Gram sums: about 256 rows each, within the partial
+      // buffer (ngroups x (nsplit + 1) matrices of kGroupMax^2).
+      const int64_t ent = (int64_t)kGroupMax * kGroupMax;
+      const int64_t cap = (int64_t)(p->sz.Zpart / 8) / (ent * ngroups) - 1;
+      if (cap < 1) {
+        // No room for the partials (tiny plans): every block on its own.
+        std::vector<Pass> single;
+        for (const Pass& ps : passes) {
+          if (ps.gi < 0) { single.push_back(ps); continue; }
+          const OrgqrGroup& g = p->groups_h[ps.gi];
+          for (int c = g.nb - 1; c >= 0; --c)
+            single.push_back(Pass{g.k0 + g.off[c], g.off[c + 1] - g.off[c], -1});
+        }
+        passes.swap(single);
+        ngroups = 0;
+      } else {
+        he = hipMemcpyAsync(p->groups_d, p->groups_h, ngroups * sizeof(OrgqrGroup),
+                            hipMemcpyHostToDevice, s);
+        if (he != hipSuccess) return hip_fail(he);
+        GroupArgs ga{};
+        ga.groups = p->groups_d; ga.ngroups = ngroups;
+        ga.V = V; ga.ldv = ldb; ga.m = m;
+        ga.Tm = Tm; ga.ldt = kTLd; ga.Tg = p->Tp; ga.ldg = kGroupMax;
+        ga.part = (double*)p->Zpart;
+        ga.nsplit = (int)std::max<int64_t>(1, std::min<int64_t>({ceil_div(gram_rows, 256), 64, cap}));
+        RRF_LAUNCH(p, RRF_STAGE_ORGQR, 2.0 * gram_rows * ent * ngroups,
+                   8.0 * gram_rows * kGroupMax * ngroups, launch_orgqr_groups(ga, s));
+      }
     }
-    for (const Group& gr : groups) {
-      const int64_t ki = gr.k0, bi = gr.b;
-      const double* Tg = gr.pair >= 0 ? p->Tp + ki * kTLd : Tm + ki * kTLd;
+    for (const Pass& ps : passes) {
+      const int64_t ki = ps.k0, bi = ps.b;
+      const double* Tg = ps.gi >= 0 ? p->Tp + ki * kGroupMax : Tm + ki * kTLd;
+      const int64_t ldt = ps.gi >= 0 ? kGroupMax : kTLd;
       if (k - ki <= 64) {
         // The last columns alone: the one-launch thin kernel.
         ThinApplyArgs ta{};
         ta.V = V + ki + ki * ldb; ta.ldv = ldb;
-        ta.Tm = Tg; ta.ldt = kTLd; ta.b = (int)bi; ta.trans = 0;
+        ta.Tm = Tg; ta.ldt = ldt; ta.b = (int)bi; ta.trans = 0;
         ta.Y = Qd + ki + ki * ldb; ta.ldy = ldb; ta.mr = m - ki; ta.ncols = (int)(k - ki);
         ta.part = p->tx; ta.sums = p->tx + kThinPartWords;
         ta.epoch_base = next_epoch(p); ta.st = p->st;
@@ -1015,8 +1072,8 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
                    launch_thin_apply(ta, p->num_cus, s));
         continue;
       }
-      rrf_status rs = apply_wy<double>(p, 0, V + ki + ki * ldb, ldb, Tg, kTLd, (int)bi,
-                                       pad16(bi), Qd + ki + ki * ldb, ldb, m - ki, k - ki,
+      rrf_status rs = apply_wy<double>(p, 0, V + ki + ki * ldb, ldb, Tg, ldt, (int)bi,
+                                       pad_group(bi), Qd + ki + ki * ldb, ldb, m - ki, k - ki,
                                        RRF_STAGE_ORGQR);
       if (rs != RRF_OK) return rs;
     }
@@ -1324,7 +1381,7 @@ rrf_status plan_create(rrf_plan_t* plan, int dtype_bits, int64_t m_max, int64_t 
   RRF_ALLOC(spec_part, p->sz.spec);
   RRF_ALLOC(Tpow, p->sz.Tpow);
   RRF_ALLOC(Tp, p->sz.Tp);
-  RRF_ALLOC(pairs_d, p->sz.pairs);
+  RRF_ALLOC(groups_d, p->sz.groups);
 #undef RRF_ALLOC
   if (e == hipSuccess) {
     ++counter;
@@ -1332,7 +1389,7 @@ rrf_status plan_create(rrf_plan_t* plan, int dtype_bits, int64_t m_max, int64_t 
     if (f && std::atoi(f) == counter) e = hipErrorOutOfMemory;
     else e = hipHostMalloc((void**)&p->st_host, sizeof(DevState), 0);
   }
-  if (e == hipSuccess) e = hipHostMalloc((void**)&p->pairs_h, p->sz.pairs, 0);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&p->groups_h, p->sz.groups, 0);
   if (e == hipSuccess) e = hipMemsetAsync(p->red, 0, p->sz.red, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->rowj, 0, p->sz.rowj, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->gx, 0, p->sz.gx, p->stream);

@@ -17,6 +17,10 @@ constexpr int kUpdRowTiles = 2;    // 16-row tiles per update wavefront
 constexpr int kUpdRows = 128;      // rows per update workgroup (4 waves x 2 x 16)
 constexpr int kUpdChunk = 16;      // columns per staged chunk in the update
 constexpr int kRedCols = 128;      // columns per reduce workgroup (4 waves x 2 x 16)
+// 16-column tiles per reduce wavefront: two, or one at 128 reflectors (whose
+// accumulators take twice the registers); a workgroup spans 64 of them.
+constexpr int red_col_tiles(int bp) { return bp == 128 ? 1 : kRedCols / 64; }
+inline int64_t red_cols(int bp) { return 64 * red_col_tiles(bp); }
 constexpr int kRedRows = 32;       // rows per staged V chunk in the reduce
 constexpr int kRedChunk = 64;      // granularity of the reduce's row splits
 constexpr int kPanelThreads = 256;
@@ -27,6 +31,8 @@ constexpr int kMaxPanelWGs = 1024;
 constexpr unsigned kSpinLimit = 1u << 24;
 
 inline int pad16(int64_t b) { return b <= 16 ? 16 : (b <= 32 ? 32 : 64); }
+// Padded width of a block of up to 128 reflectors (the explicit-Q pass).
+inline int pad_group(int64_t b) { return b <= 64 ? pad16(b) : 128; }
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 
@@ -183,19 +189,32 @@ struct GramPanelArgs {
 bool gram_panel_shape(int64_t m, int b, int num_cus, PanelShape* out);
 hipError_t launch_panel_gram(const GramPanelArgs& a, const PanelShape& sh, hipStream_t s);
 
-// Explicit-Q pass: two adjacent blocks of 16..32 reflectors each applied as
-// one block (orgqr_pairs.hip).  Per pair: k0, the first column, b1 and b2
-// the widths.  part holds npairs x nsplit x 32 x 32 doubles; the merged T
-// of the pair at column k0 goes to Tp + k0 ldt (64 x 64, ld ldt).
-struct OrgqrPair { int64_t k0; int b1, b2; };
-struct PairArgs {
-  const OrgqrPair* pairs;
+// Explicit-Q pass: adjacent blocks of reflectors applied as one block of up
+// to kGroupMax (orgqr_groups.hip).  Per group: k0, the first column; nb
+// blocks at column offsets off[0] = 0 < off[1] < ... < off[nb] = w; the
+// 16 x 16 tiles (ti, tj) of the Gram matrix V^T V that the merge reads
+// (tile[n] = 8 ti + tj, those holding an entry (i, j) with block(i) <
+// block(j)).  part holds ngroups x nsplit partial Gram matrices, then
+// ngroups sums (each kGroupMax^2 doubles, only the listed tiles written);
+// the merged T of the group at column k0 goes to Tg + k0 ldg (w x w,
+// ldg >= kGroupMax).  Tm, ldt: the blocks' own T.
+constexpr int kGroupMax = 128;
+constexpr int kMaxGroupBlocks = 8;
+constexpr int kGroupTiles = (kGroupMax / 16) * (kGroupMax / 16);
+struct OrgqrGroup {
+  int64_t k0;
+  int nb, w, ntiles;
+  int off[kMaxGroupBlocks + 1];
+  unsigned char tile[kGroupTiles];
+};
+struct GroupArgs {
+  const OrgqrGroup* groups; int ngroups;
   double* V; int64_t ldv; int64_t m;
   const double* Tm; int64_t ldt;
-  double* Tp;
+  double* Tg; int64_t ldg;
   double* part; int nsplit;
 };
-hipError_t launch_orgqr_pairs(const PairArgs& a, int npairs, hipStream_t s);
+hipError_t launch_orgqr_groups(const GroupArgs& a, hipStream_t s);
 
 // Y <- Y - V T^T (V^T Y) for a thin Y (mr x ncols, ncols <= 64), binary64,
 // one launch (reflectors p >= b and columns >= ncols are

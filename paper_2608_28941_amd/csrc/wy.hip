@@ -33,7 +33,7 @@ namespace {
 
 // ---------------------------------------------------------------------------
 // reduce: Z_s[c * BP + p] = sum_{r in split s} V[r, p] X[r, c]
-// grid (ceil(n / kRedCols), nsplit), 256 threads; V is staged in chunks of
+// grid (ceil(n / (64 CT)), nsplit), 256 threads; V is staged in chunks of
 // RC rows.
 //
 // An MFMA operand puts the summation index (rows of X) on the 4 lane groups
@@ -62,7 +62,7 @@ __global__ __launch_bounds__(256, 2) void reduce_kernel(ReduceArgs<T> a) {
   constexpr int NIT = (BP * RC) / 256;     // V values per thread per chunk
   static_assert(RC % GR == 0 && kRedChunk % RC == 0 && 256 % RC == 0 &&
                 (BP * RC) % 256 == 0, "chunk shape");
-  static_assert(kRedCols == 64 * CT, "workgroup width");
+  constexpr int COLS = 64 * CT;            // columns per workgroup
   // Staged V rows, double buffered (chunk c in buffer c % 2): one barrier per
   // chunk orders the reads of a buffer before its next overwrite and the
   // writes before the next reads.
@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256, 2) void reduce_kernel(ReduceArgs<T> a) {
   const int m16 = lane & 15, g = lane >> 4;
   // Wavefront w owns CT adjacent 16-column tiles; every staged V value read
   // from LDS feeds CT MFMAs.
-  const int64_t cb = (int64_t)blockIdx.x * kRedCols + 16 * CT * wave;
+  const int64_t cb = (int64_t)blockIdx.x * COLS + 16 * CT * wave;
   const int64_t r_begin = (int64_t)blockIdx.y * a.rows_per_split;
   const int64_t r_end = min(a.mr, r_begin + a.rows_per_split);
   const T* Xc[CT];
@@ -228,12 +228,20 @@ __global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
     }
     zs[cl][p] = c < a.n ? z : 0.0;
     __syncthreads();
-    double w = 0.0;
+    // Four independent partial sums (the terms past the triangle are zero in
+    // Tl), added in a fixed order.
+    double w4[4] = {0.0, 0.0, 0.0, 0.0};
     if (a.trans) {
-      for (int l = 0; l <= p; ++l) w += Tl[l][p] * zs[cl][l];
+      for (int l = 0; l <= p; l += 4)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (l + u < BP) w4[u] += Tl[l + u][p] * zs[cl][l + u];
     } else {
-      for (int l = p; l < BP; ++l) w += Tl[p][l] * zs[cl][l];
+      for (int l = p & ~3; l < BP; l += 4)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) w4[u] += Tl[p][l + u] * zs[cl][l + u];
     }
+    const double w = (w4[0] + w4[1]) + (w4[2] + w4[3]);
     if (c < n_pad) a.W[c * BP + p] = (T)w;
   }
 }
@@ -254,23 +262,32 @@ hipError_t upd_go(const UpdateArgs<T>& a, dim3 grid, hipStream_t s) {
 
 template <typename T, int BP>
 hipError_t upd_q(const UpdateArgs<T>& a, dim3 grid, hipStream_t s) {
-  switch (a.qp) {
-    case 0: return upd_go<T, BP, 0>(a, grid, s);
-    case 16: return upd_go<T, BP, 16>(a, grid, s);
-    case 32: return upd_go<T, BP, 32>(a, grid, s);
-    case 64: return upd_go<T, BP, 64>(a, grid, s);
+  if constexpr (BP == 128) {
+    // 128 reflectors: the explicit-Q pass only (binary64, no sample).
+    if constexpr (std::is_same<T, double>::value) {
+      if (a.qp == 0) return upd_go<T, 128, 0>(a, grid, s);
+    }
+    return hipErrorInvalidValue;
+  } else {
+    switch (a.qp) {
+      case 0: return upd_go<T, BP, 0>(a, grid, s);
+      case 16: return upd_go<T, BP, 16>(a, grid, s);
+      case 32: return upd_go<T, BP, 32>(a, grid, s);
+      case 64: return upd_go<T, BP, 64>(a, grid, s);
+    }
+    return hipErrorInvalidValue;
   }
-  return hipErrorInvalidValue;
 }
 
 template <typename T, int BP>
-hipError_t red_go(const ReduceArgs<T>& a, dim3 grid, hipStream_t s) {
+hipError_t red_go(const ReduceArgs<T>& a, int nsplit, hipStream_t s) {
   // 16-byte packs of X when the region is aligned to them.
   constexpr int VEC = 16 / (int)sizeof(T);
   const bool vec_ok = (reinterpret_cast<uintptr_t>(a.X) % 16) == 0 &&
                       a.ldx % VEC == 0 && a.mr % VEC == 0 &&
                       a.rows_per_split % VEC == 0;
-  constexpr int CT = kRedCols / 64;
+  constexpr int CT = red_col_tiles(BP);
+  const dim3 grid((unsigned)ceil_div(a.n, 64 * CT), (unsigned)nsplit);
   if (vec_ok)
     hipLaunchKernelGGL((reduce_kernel<T, BP, VEC, CT, kRedRows>), grid, dim3(256), 0, s, a);
   else
@@ -293,6 +310,7 @@ hipError_t launch_update(const UpdateArgs<T>& a, int nsplit, hipStream_t s) {
     case 16: return upd_q<T, 16>(a, grid, s);
     case 32: return upd_q<T, 32>(a, grid, s);
     case 64: return upd_q<T, 64>(a, grid, s);
+    case 128: return upd_q<T, 128>(a, grid, s);
   }
   return hipErrorInvalidValue;
 }
@@ -300,11 +318,13 @@ hipError_t launch_update(const UpdateArgs<T>& a, int nsplit, hipStream_t s) {
 template <typename T>
 hipError_t launch_reduce(const ReduceArgs<T>& a, int nsplit, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
-  dim3 grid((unsigned)ceil_div(a.n, kRedCols), (unsigned)nsplit);
   switch (a.bp) {
-    case 16: return red_go<T, 16>(a, grid, s);
-    case 32: return red_go<T, 32>(a, grid, s);
-    case 64: return red_go<T, 64>(a, grid, s);
+    case 16: return red_go<T, 16>(a, nsplit, s);
+    case 32: return red_go<T, 32>(a, nsplit, s);
+    case 64: return red_go<T, 64>(a, nsplit, s);
+    case 128:
+      if constexpr (std::is_same<T, double>::value) return red_go<T, 128>(a, nsplit, s);
+      break;
   }
   return hipErrorInvalidValue;
 }
@@ -314,12 +334,21 @@ hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   const int cpb = 256 / a.bp;
   int64_t blocks = ceil_div(a.n, cpb);
-  if (blocks > 2048) blocks = 2048;
+  // Every workgroup stages all of T (bp^2 values): at 128 reflectors fewer
+  // workgroups, each over more columns, keep that re-read small.
+  const int64_t cap = a.bp == 128 ? 256 : 2048;
+  if (blocks > cap) blocks = cap;
   dim3 grid((unsigned)blocks);
   switch (a.bp) {
     case 16: hipLaunchKernelGGL((formw_kernel<T, 16>), grid, dim3(256), 0, s, a); break;
     case 32: hipLaunchKernelGGL((formw_kernel<T, 32>), grid, dim3(256), 0, s, a); break;
     case 64: hipLaunchKernelGGL((formw_kernel<T, 64>), grid, dim3(256), 0, s, a); break;
+    case 128:
+      if constexpr (std::is_same<T, double>::value) {
+        hipLaunchKernelGGL((formw_kernel<T, 128>), grid, dim3(256), 0, s, a);
+        break;
+      }
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
