@@ -44,13 +44,13 @@ constexpr int kTLd = 64;          // T stored like geqrt's T: 64 rows
 struct Sizes {
   int64_t ldb, kcap, kcols;
   int64_t ldysum;
-  size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, red,
+  size_t Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64, normpart, normtag, red,
       rowj, st, trace, tsqr, gx, tx, Yest, spec, Tpow, Tp, groups;
   // Every buffer at a 256-byte boundary (a caller-provided workspace is
   // carved in this order).
   size_t total() const {
     const size_t parts[] = {Bws, V, Tm, tau, Ypart, Ysum, Om, Zpart, W, Q, Q64,
-                            normpart, tsqr, red, rowj, gx, tx, st, trace / 3,
+                            normpart, normtag, tsqr, red, rowj, gx, tx, st, trace / 3,
                             trace / 3, trace / 3, Yest, spec, Tpow, Tp, groups};
     size_t t = 0;
     for (size_t x : parts)
@@ -84,6 +84,9 @@ Sizes compute_sizes(rrf_dtype dt, int64_t m_max, int64_t n_max, int64_t b_max,
   z.Q = (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * e;
   z.Q64 = dt == RRF_F32 ? (size_t)z.ldb * std::max<int64_t>(z.kcap, 1) * 8 : 0;
   z.normpart = (size_t)(ceil_div(m_max, kUpdRows) * kMaxUpdSplits + 1) * 2 * 8;
+  // The same partials as epoch-tagged words (two per value), when the
+  // update's last workgroup finalizes.
+  z.normtag = z.normpart * 2;
   // Panel partials: two epoch-tagged 64-bit words per value.
   z.red = (size_t)2 * kMaxPanelWGs * 64 * 2 * 8;
   z.rowj = (size_t)2 * 64 * 2 * 8;
@@ -139,6 +142,7 @@ struct rrf_plan {
   int panel_mode;            // kPanelGrid, kPanelTsqr, kPanelGram or kPanelAuto
   double *V, *Tm, *tau, *Ysum;
   double *normpart, *trace_trail_d, *trace_sub_d, *trace_spec_d;
+  unsigned long long* normtag;   // tagged norm partials (finalisation in the update)
   double *Yest, *spec_part, *Tpow;
   int power;                 // power iterations per block sample
   unsigned long long *red, *rowj, *gx, *tx;
@@ -436,6 +440,21 @@ rrf_status apply_wy(rrf_plan* p, int trans, const double* V, int64_t ldv,
   return RRF_OK;
 }
 
+// The update launch u finalizes its own norm partials (the stop test of
+// the finalize kernel, in its last workgroup): nparts update workgroups,
+// trace index block (< 0: none), init for the first sample.
+template <typename T>
+void set_finalize(rrf_plan* p, UpdateArgs<T>& u, int nparts, int block, int64_t k_after,
+                  int64_t k_cap, int mode, double tol, int init) {
+  u.normtag = p->normtag;
+  u.fin_epoch = next_epoch(p) + 1u;
+  u.fin_nwg = nparts;
+  FinalizeArgs& f = u.fin;
+  f.nparts = nparts; f.st = p->st; f.tt = p->trace_trail_d; f.ts = p->trace_sub_d;
+  f.block = block; f.k_after = k_after; f.k_cap = k_cap; f.mode = mode; f.tol = tol;
+  f.init = init;
+}
+
 template <typename T>
 rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
                     double tol, int64_t b, uint64_t seed, int64_t* k_out,
@@ -522,6 +541,12 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     rrf_status rs = sketch_window(0, q0, &om_win);
     if (rs != RRF_OK) return rs;
   }
+  // A wait error left by an earlier call is cleared before the first launch
+  // (the first sample's finalisation waits on the tagged norm partials).
+  {
+    hipError_t he0 = clear_wait_error(p);
+    if (he0 != hipSuccess) return hip_fail(he0);
+  }
   UpdateArgs<T> u{};
   u.src = A; u.lds = lda; u.dst = nullptr; u.ldd = 0; u.mr = m; u.n = n;
   u.V = nullptr; u.ldv = 0; u.bp = 0; u.W = nullptr; u.ldw = 0;
@@ -532,14 +557,14 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     u.cols_per_split = round_up(ceil_div(n, su0), 2 * kUpdChunk);
   }
   int ysplits = (int)ceil_div(n, u.cols_per_split);
+  int nparts = (int)(ceil_div(m, kUpdRows) * ysplits);
+  // E0 and sigma^2 from the sample's own launch (its last workgroup).
+  set_finalize(p, u, nparts, -1, 0, kcap, mode, tol, 1);
   RRF_LAUNCH(p, RRF_STAGE_SAMPLE, 2.0 * m * n * b0, e * (m * n + m * b0),
              launch_update<T>(u, ysplits, s));
-  int nparts = (int)(ceil_div(m, kUpdRows) * ysplits);
-  RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
-             launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
-                             p->trace_sub_d, 0, 0, kcap, mode, tol, 1, s));
   hipError_t he = read_state(p);
   if (he != hipSuccess) return hip_fail(he);
+  if (p->st_host->barrier_err) return RRF_ERR_INTERNAL;
   if (p->st_host->nonfinite) return RRF_ERR_NONFINITE;
   const int power = p->power;
   if (power > 0)
@@ -841,6 +866,12 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     const int su = (int)ceil_div(n, ua.cols_per_split);
     const double smp_flops = 2.0 * (mp - bi) * n * b_s;
     const double upd_flops = 2.0 * mp * n * bi + smp_flops;
+    nparts = (int)(ceil_div(mp, kUpdRows) * su);
+    // The stop test runs in the update's last workgroup, except where the
+    // spectral estimate of the next block comes between them.
+    const bool fin_in_update = !(mode == RRF_STOP_SPECTRAL && at_end && b_next > 0);
+    if (fin_in_update)
+      set_finalize(p, ua, nparts, at_end ? blk : -1, k_next, kcap, mode, tol, 0);
     if (panel_ready) {
       pan.epoch_base = next_epoch(p);
       if (fused && la_gram) {
@@ -884,11 +915,11 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       rrf_status rs = spectral(k_next, b_next, Yy, p->sz.ldysum, blk);
       if (rs != RRF_OK) return rs;
     }
-    nparts = (int)(ceil_div(mp, kUpdRows) * su);
-    RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
-               launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
-                               p->trace_sub_d, at_end ? blk : -1, k_next, kcap,
-                               mode, tol, 0, s));
+    if (!fin_in_update)
+      RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
+                 launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
+                                 p->trace_sub_d, at_end ? blk : -1, k_next, kcap,
+                                 mode, tol, 0, s));
     if (!at_end) {
       // Inside a block: the next sub-block runs whatever the norms say (an
       // error recorded meanwhile is read at the end of the block).
@@ -1368,6 +1399,7 @@ rrf_status plan_create(rrf_plan_t* plan, int dtype_bits, int64_t m_max, int64_t 
   RRF_ALLOC(Q, p->sz.Q);
   if (p->sz.Q64) RRF_ALLOC(Q64, p->sz.Q64);
   RRF_ALLOC(normpart, p->sz.normpart);
+  RRF_ALLOC(normtag, p->sz.normtag);
   RRF_ALLOC(tsqr, p->sz.tsqr);
   RRF_ALLOC(red, p->sz.red);
   RRF_ALLOC(rowj, p->sz.rowj);
@@ -1394,6 +1426,7 @@ rrf_status plan_create(rrf_plan_t* plan, int dtype_bits, int64_t m_max, int64_t 
   if (e == hipSuccess) e = hipMemsetAsync(p->rowj, 0, p->sz.rowj, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->gx, 0, p->sz.gx, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->tx, 0, p->sz.tx, p->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(p->normtag, 0, p->sz.normtag, p->stream);
   if (e == hipSuccess) {
     std::memset(p->st_host, 0, sizeof(DevState));
     p->st_host->spin_limit = p->spin_limit;

@@ -1,68 +1,15 @@
 // Small kernels: residual-norm finalisation and stop test (Alg. 2 E update
 // and loop condition), identity fill for the explicit Q, copies.
 
+#include "finalize_body.h"
 #include "rrf_internal.h"
 
 namespace rrf {
 namespace {
 
-// Sums the per-workgroup norm partials in a fixed order (deterministic) and
-// applies the stop test.  init: E0 = ||A||_F^2, sigma^2 = tol^2 E0.
-// Otherwise: E_trail = ||B[k:m, :]||^2 directly, E_sub -= ||B_i||^2 (the
-// paper's running difference, clamped at 0); in spectral mode (2) the
-// estimate the spectral kernels left in the run state.  At the end of a block (block
-// >= 0: the trace index) the stop test runs: stop iff E <= sigma^2 or the
-// rank cap is reached (Sec. 4: the loop ends after at most min(m, n) / b
-// blocks); inside a block (block < 0, the first 64 columns of a wider
-// block) only errors stop.  A NaN norm fails "E > sigma^2" and would stop
-// silently, so non-finite norms are flagged.
-__global__ __launch_bounds__(256) void finalize_kernel(
-    const double* np, int nparts, DevState* st, double* tt, double* ts,
-    int block, int64_t k_after, int64_t k_cap, int mode, double tol, int init) {
-  __shared__ double sb[256], stl[256];
-  double a = 0.0, c = 0.0;
-  for (int i = threadIdx.x; i < nparts; i += 256) {
-    a += np[2 * i + 0];
-    c += np[2 * i + 1];
-  }
-  sb[threadIdx.x] = a;
-  stl[threadIdx.x] = c;
-  __syncthreads();
-  for (int h = 128; h > 0; h >>= 1) {
-    if (threadIdx.x < h) {
-      sb[threadIdx.x] += sb[threadIdx.x + h];
-      stl[threadIdx.x] += stl[threadIdx.x + h];
-    }
-    __syncthreads();
-  }
-  if (threadIdx.x != 0) return;
-  const double blk = sb[0], trail = stl[0];
-  if (init) {
-    const double E0 = blk + trail;
-    st->E0 = E0;
-    st->nonfinite = !isfinite(E0);
-    st->sigma2 = (tol * tol) * E0;
-    st->E_trail = E0;
-    st->E_sub = E0;
-    st->E_spec = E0;
-    st->stop = st->nonfinite || !(E0 > st->sigma2) || k_cap == 0;
-    st->barrier_err = 0;
-  } else {
-    double es = st->E_sub - blk;
-    if (es < 0.0) es = 0.0;
-    st->E_sub = es;
-    st->E_trail = trail;
-    if (!isfinite(trail)) st->nonfinite = 1;
-    if (block >= 0) {
-      tt[block] = trail;
-      ts[block] = es;
-      const double E = mode == 0 ? trail : (mode == 1 ? es : st->E_spec);
-      st->stop = st->nonfinite || st->barrier_err || !(E > st->sigma2) ||
-                 k_after >= k_cap;
-    } else {
-      st->stop = st->nonfinite || st->barrier_err;
-    }
-  }
+// The one-workgroup finalisation (finalize_body.h) from plain partials.
+__global__ __launch_bounds__(256) void finalize_kernel(const double* np, FinalizeArgs f) {
+  finalize_plain(np, f);
 }
 
 template <typename T>
@@ -97,9 +44,10 @@ hipError_t launch_finalize(const double* normpart, int nparts, DevState* st,
                            double* trace_trail, double* trace_sub, int block,
                            int64_t k_after, int64_t k_cap, int mode,
                            double tol, int init, hipStream_t s) {
-  hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(256), 0, s, normpart,
-                     nparts, st, trace_trail, trace_sub, block, k_after, k_cap,
-                     mode, tol, init);
+  FinalizeArgs f{};
+  f.nparts = nparts; f.st = st; f.tt = trace_trail; f.ts = trace_sub; f.block = block;
+  f.k_after = k_after; f.k_cap = k_cap; f.mode = mode; f.tol = tol; f.init = init;
+  hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(256), 0, s, normpart, f);
   return hipGetLastError();
 }
 

@@ -52,6 +52,20 @@ struct DevState {
 
 // Launch descriptors -------------------------------------------------------
 
+// Residual-norm finalisation and stop test of one launch's norm partials
+// (finalize_body.h): nparts parts; traces tt, ts at index block (< 0: inside
+// a block, no trace and no stop test but on errors); init: the first sample.
+struct FinalizeArgs {
+  int nparts;
+  DevState* st;
+  double* tt; double* ts;
+  int block;
+  int64_t k_after, k_cap;
+  int mode;
+  double tol;
+  int init;
+};
+
 template <typename T>
 struct UpdateArgs {
   const T* src; int64_t lds;   // region rows start at the pointer
@@ -66,6 +80,14 @@ struct UpdateArgs {
   int64_t s0;                  // rows < s0: block-row norm; >= s0: trailing norm
   double* normpart;            // 2 doubles per workgroup, or nullptr
   int64_t cols_per_split;
+  // Optional (normtag != nullptr, with normpart): the norm partials are
+  // published as epoch-tagged words (4 per workgroup, epoch fin_epoch)
+  // instead, and the last of the fin_nwg update workgroups (the last one
+  // dispatched) waits for them and runs the finalisation fin.
+  unsigned long long* normtag;
+  unsigned fin_epoch;
+  int fin_nwg;
+  FinalizeArgs fin;
 };
 
 template <typename T>

@@ -7,6 +7,7 @@
 
 #include <type_traits>
 
+#include "finalize_body.h"
 #include "mfma.h"
 #include "rrf_internal.h"
 
@@ -91,11 +92,23 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
   const int m16 = lane & 15, g = lane >> 4;
   const int64_t cs = (int64_t)split * a.cols_per_split;
   const int64_t ce = min(a.n, cs + a.cols_per_split);
-  if (cs >= ce) {          // empty split (uniform per workgroup, before any barrier)
-    if (a.normpart && threadIdx.x == 0) {
-      a.normpart[2 * ((int64_t)split * nrb + rb) + 0] = 0.0;
-      a.normpart[2 * ((int64_t)split * nrb + rb) + 1] = 0.0;
+  // This workgroup's norm partials (thread 0's values): plain, or tagged with
+  // the finalisation in the last update workgroup.
+  auto publish = [&](const double nbv, const double ntv) {
+    const int64_t wg = (int64_t)split * nrb + rb;
+    if (a.normtag) {
+      if (threadIdx.x == 0) {
+        put_tagged(&a.normtag[4 * wg], nbv, a.fin_epoch);
+        put_tagged(&a.normtag[4 * wg + 2], ntv, a.fin_epoch);
+      }
+      if (wg == a.fin_nwg - 1) finalize_tagged(a.normtag, a.fin_epoch, a.fin);   // uniform
+    } else if (threadIdx.x == 0) {
+      a.normpart[2 * wg + 0] = nbv;
+      a.normpart[2 * wg + 1] = ntv;
     }
+  };
+  if (cs >= ce) {          // empty split (uniform per workgroup, before any barrier)
+    if (a.normpart) publish(0.0, 0.0);
     return;
   }
   int64_t r[RT];
@@ -331,11 +344,8 @@ __device__ __forceinline__ void update_body(const UpdateArgs<T>& a, const unsign
       nred[1][wave] = nt;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-      const int64_t wg = (int64_t)split * nrb + rb;
-      a.normpart[2 * wg + 0] = ((nred[0][0] + nred[0][1]) + nred[0][2]) + nred[0][3];
-      a.normpart[2 * wg + 1] = ((nred[1][0] + nred[1][1]) + nred[1][2]) + nred[1][3];
-    }
+    publish(((nred[0][0] + nred[0][1]) + nred[0][2]) + nred[0][3],
+            ((nred[1][0] + nred[1][1]) + nred[1][2]) + nred[1][3]);
   }
 }
 
