@@ -253,8 +253,42 @@ int red_splits(int64_t mr, int64_t n, int num_cus) {
 // dependent chunks, so short splits keep a narrow reduce off the latency of
 // that chain.
 constexpr int kNarrowRows = 32;
+
+// Splits of a length len (in multiples of gran) into s parts, each part
+// `other` workgroups wide, on `slots` resident workgroups: the s in [1, smax]
+// that minimises rounds x (part length + one granule of per-workgroup
+// set-up), fewest splits on ties (a nearly empty last round costs as much as
+// a full one).
+int64_t splits_by_rounds(int64_t other, int64_t len, int64_t gran, int64_t slots,
+                         int64_t smax) {
+  other = std::max<int64_t>(other, 1);
+  slots = std::max<int64_t>(slots, 1);
+  int64_t best = 1, best_cost = INT64_MAX;
+  for (int64_t s = 1; s <= std::max<int64_t>(smax, 1); ++s) {
+    const int64_t cost =
+        ceil_div(other * s, slots) * (round_up(ceil_div(len, s), gran) + gran);
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = s;
+    }
+  }
+  return best;
+}
+
+// Both 128-reflector kernels of the explicit-Q pass (reduce and update) hold
+// two workgroups per compute unit: their LDS and VGPR use allow no more.
+constexpr int kWide128PerCu = 2;
+
 int red_splits_narrow(int64_t mr, int64_t n, int bp, int num_cus, int64_t max_splits) {
   const int64_t col_wgs = ceil_div(n, red_cols(bp));
+  if (bp == 128) {
+    // Never more than one round's worth: each split adds a partial for
+    // formW to read.
+    const int64_t slots = (int64_t)kWide128PerCu * num_cus;
+    return (int)splits_by_rounds(col_wgs, mr, kNarrowRows, slots,
+                                 std::min<int64_t>({ceil_div(slots, col_wgs), 128, max_splits,
+                                                    std::max<int64_t>(1, mr / kNarrowRows)}));
+  }
   int64_t s = ceil_div(2 * (int64_t)num_cus, std::max<int64_t>(col_wgs, 1));
   s = std::min<int64_t>({s, 128, max_splits, std::max<int64_t>(1, mr / kNarrowRows)});
   // At 128 reflectors two workgroups per compute unit are the whole target:
@@ -433,6 +467,12 @@ rrf_status apply_wy(rrf_plan* p, int trans, const double* V, int64_t ldv,
     const int64_t row_wgs = std::max<int64_t>(ceil_div(mr, kUpdRows), 1);
     int64_t su0 = ceil_div(4 * (int64_t)p->num_cus, row_wgs);
     su0 = std::max<int64_t>(1, std::min<int64_t>({su0, ncols / 32, 64}));
+    // At 128 reflectors, whole rounds over the two resident workgroups per
+    // compute unit.
+    if (bp == 128)
+      su0 = splits_by_rounds(row_wgs, ncols, 2 * kUpdChunk,
+                             (int64_t)kWide128PerCu * p->num_cus,
+                             std::max<int64_t>(1, std::min<int64_t>(ncols / 32, 64)));
     ua.cols_per_split = round_up(ceil_div(ncols, su0), 2 * kUpdChunk);
   }
   const int su = (int)ceil_div(ncols, ua.cols_per_split);
