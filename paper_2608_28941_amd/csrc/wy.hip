@@ -246,6 +246,100 @@ __global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
   }
 }
 
+// formW at 128 reflectors, W = T z_c (the explicit-Q pass of a block group):
+// one workgroup per tile of CW columns (CW = 4, 8 or 16, chosen so that
+// narrow passes still spread over many compute units).
+// * The tile's split partials are summed in split order, as in formw_kernel,
+//   16 loads of 16 bytes in flight per thread, and z goes to LDS.
+// * The product with the upper b x b triangle of T runs on MFMA 16x16x4:
+//   D rows are the tile's columns c (rows >= CW zero), D columns 16 values
+//   of p, K the index l.  Wave w takes the p-tiles w and 7 - w, 36 K-steps
+//   of 4 between them (l >= p, so tile pt needs l >= 16 pt only).
+// * Its T operand, T[p][l] with p <= l < b, is loaded at the start, beside
+//   the partials.
+template <int CW>
+__global__ __launch_bounds__(256) void formw128_kernel(FormWArgs<double> a) {
+  constexpr int BP = 128;
+  constexpr int PK = CW * BP / 2 / 256;  // 16-byte packs per thread per split
+  constexpr int SB = 16 / PK;            // splits in flight
+  constexpr int NS = 36;                 // K-steps per wave
+  __shared__ double zs[16][BP + 1];
+  const int t = threadIdx.x, w = t >> 6, lane = t & 63, g = lane >> 4, m = lane & 15;
+  const int64_t c0 = (int64_t)blockIdx.x * CW;
+  // T operand: steps [0, nA) belong to p-tile w, the rest to p-tile 7 - w.
+  const int nA = 32 - 4 * w;
+  double bv[NS];
+#pragma unroll
+  for (int st = 0; st < NS; ++st) {
+    const bool inA = st < nA;
+    const int pt = inA ? w : 7 - w;
+    const int l = 16 * pt + 4 * (inA ? st : st - nA) + g;
+    const int p = 16 * pt + m;
+    bv[st] = (p <= l && l < a.b) ? a.Tm[p + (int64_t)l * a.ldt] : 0.0;
+  }
+  // Split sums: pack q = t + 256 j covers z[c0 + q / 64][2 (q % 64) + {0, 1}].
+  double2 z[PK];
+  const double2* zp[PK];
+  bool ok[PK];
+#pragma unroll
+  for (int j = 0; j < PK; ++j) {
+    const int q = t + 256 * j;
+    const int64_t c = c0 + q / 64;
+    ok[j] = c < a.n;
+    zp[j] = reinterpret_cast<const double2*>(a.Z + (ok[j] ? c : 0) * BP + 2 * (q % 64));
+    z[j] = make_double2(0.0, 0.0);
+  }
+  const int64_t ss = a.split_stride / 2;  // in packs
+  for (int s0 = 0; s0 < a.nsplit; s0 += SB) {
+    double2 v[SB][PK];
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const int64_t su = min(s0 + u, a.nsplit - 1);
+#pragma unroll
+      for (int j = 0; j < PK; ++j) v[u][j] = zp[j][su * ss];
+    }
+#pragma unroll
+    for (int u = 0; u < SB; ++u)
+      if (s0 + u < a.nsplit)
+#pragma unroll
+        for (int j = 0; j < PK; ++j) {
+          z[j].x += v[u][j].x;
+          z[j].y += v[u][j].y;
+        }
+  }
+#pragma unroll
+  for (int j = 0; j < PK; ++j) {
+    const int q = t + 256 * j;
+    zs[q / 64][2 * (q % 64) + 0] = ok[j] ? z[j].x : 0.0;
+    zs[q / 64][2 * (q % 64) + 1] = ok[j] ? z[j].y : 0.0;
+  }
+  __syncthreads();
+  d4_t accA = Mfma<double>::zero(), accB = Mfma<double>::zero();
+#pragma unroll
+  for (int st = 0; st < NS; ++st) {
+    const bool inA = st < nA;
+    const int pt = inA ? w : 7 - w;
+    const int l = 16 * pt + 4 * (inA ? st : st - nA) + g;
+    const double av = m < CW ? zs[m][l] : 0.0;
+    if (inA)
+      accA = Mfma<double>::op(av, bv[st], accA);
+    else
+      accB = Mfma<double>::op(av, bv[st], accB);
+  }
+  // Lane (g, m), item i: W[c0 + g + 4 i][16 pt + m]; rows [n, n_pad) get the
+  // zeros of their zero z.
+  const int64_t n_pad = (a.n + kUpdChunk - 1) / kUpdChunk * kUpdChunk;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = Mfma<double>::drow(g, i);
+    const int64_t c = c0 + r;
+    if (r < CW && c < n_pad) {
+      a.W[c * BP + 16 * w + m] = accA[i];
+      a.W[c * BP + 16 * (7 - w) + m] = accB[i];
+    }
+  }
+}
+
 template <typename T, int BP, int QP, bool STORE>
 __global__ __launch_bounds__(256, 2) void update_kernel(UpdateArgs<T> a) {
   update_body<T, BP, QP, STORE>(a, blockIdx.x, blockIdx.y, gridDim.x);
@@ -345,6 +439,23 @@ hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s) {
     case 64: hipLaunchKernelGGL((formw_kernel<T, 64>), grid, dim3(256), 0, s, a); break;
     case 128:
       if constexpr (std::is_same<T, double>::value) {
+        if (!a.trans) {
+          // The widest tile that still gives half the compute units a
+          // workgroup; the partials are 16-byte packs.
+          if (reinterpret_cast<uintptr_t>(a.Z) % 16 != 0 || a.split_stride % 2 != 0)
+            return hipErrorInvalidValue;
+          const int64_t n_pad = ceil_div(a.n, kUpdChunk) * kUpdChunk;
+          if (ceil_div(n_pad, 16) >= 128)
+            hipLaunchKernelGGL((formw128_kernel<16>), dim3((unsigned)ceil_div(n_pad, 16)),
+                               dim3(256), 0, s, a);
+          else if (ceil_div(n_pad, 8) >= 128)
+            hipLaunchKernelGGL((formw128_kernel<8>), dim3((unsigned)ceil_div(n_pad, 8)),
+                               dim3(256), 0, s, a);
+          else
+            hipLaunchKernelGGL((formw128_kernel<4>), dim3((unsigned)ceil_div(n_pad, 4)),
+                               dim3(256), 0, s, a);
+          break;
+        }
         hipLaunchKernelGGL((formw_kernel<T, 128>), grid, dim3(256), 0, s, a);
         break;
       }
