@@ -28,6 +28,9 @@ constexpr int kThinSlots = 16 * 256;   // 64 x 64 values in MFMA tile order (at 
 // Rows of a chunk staged in LDS (V and Y, 64 columns each).
 constexpr int kThinChunk = 64;
 
+// TM: 16 x 16 tiles per side that the MFMA loops cover (2: b and ncols at
+// most 32; 4: up to 64); the tiles past it are zero and are not computed.
+template <int TM>
 __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
   __shared__ double Vs[kThinChunk][65];
   __shared__ double Ys[kThinChunk][65];
@@ -96,18 +99,20 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
     __syncthreads();
     stage(r0);
     __syncthreads();
+    if (wv < TM) {
 #pragma unroll 4
-    for (int s4 = 0; s4 < kThinChunk / 4; ++s4) {
-      const double av = Vs[4 * s4 + l16][16 * wv + m16];
+      for (int s4 = 0; s4 < kThinChunk / 4; ++s4) {
+        const double av = Vs[4 * s4 + l16][16 * wv + m16];
 #pragma unroll
-      for (int ct = 0; ct < 4; ++ct)
-        acc[ct] = Mfma<double>::op(av, Ys[4 * s4 + l16][16 * ct + m16], acc[ct]);
+        for (int ct = 0; ct < TM; ++ct)
+          acc[ct] = Mfma<double>::op(av, Ys[4 * s4 + l16][16 * ct + m16], acc[ct]);
+      }
     }
   }
   if (wv < PT) {
     u64* dst = a.part + (int64_t)w * NS * 2;
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
+    for (int ct = 0; ct < TM; ++ct)
       if (ct < CT) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -162,7 +167,7 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
   //    holds Z[16 pt + lane/16 + 4 i][16 ct + lane%16]; tiles not exchanged
   //    are zero (reflectors >= b and columns >= ncols contribute nothing).
   {
-    constexpr int NPT = kThinSlots / 256;
+    constexpr int NPT = TM * TM;
     const int nq = NS / 256;
     u64 hi[NPT], lo[NPT];
     unsigned spins = 0;
@@ -198,16 +203,19 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
   // tile (pt = wave, ct), A[m][k] = T[k][16 pt + m] (or T[16 pt + m][k]),
   // B[k][n] = Z[k][16 ct + n], into registers, then over Z.
   {
+    // Rows of W past 16 TM are zero (T is), as are the terms k >= 16 TM.
     d4_t wacc[4];
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) wacc[ct] = d4_t{0.0, 0.0, 0.0, 0.0};
+    if (wv < TM) {
 #pragma unroll
-    for (int s4 = 0; s4 < 16; ++s4) {
-      const double av = a.trans ? Tl[4 * s4 + l16][16 * wv + m16]
-                                : Tl[16 * wv + m16][4 * s4 + l16];
+      for (int s4 = 0; s4 < 4 * TM; ++s4) {
+        const double av = a.trans ? Tl[4 * s4 + l16][16 * wv + m16]
+                                  : Tl[16 * wv + m16][4 * s4 + l16];
 #pragma unroll
-      for (int ct = 0; ct < 4; ++ct)
-        wacc[ct] = Mfma<double>::op(av, ZW[4 * s4 + l16][16 * ct + m16], wacc[ct]);
+        for (int ct = 0; ct < TM; ++ct)
+          wacc[ct] = Mfma<double>::op(av, ZW[4 * s4 + l16][16 * ct + m16], wacc[ct]);
+      }
     }
     __syncthreads();
 #pragma unroll
@@ -226,13 +234,13 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
     const int rrow = 16 * wv + m16;
     const int64_t r = r0 + rrow;
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
+    for (int ct = 0; ct < TM; ++ct) {
       if (16 * ct >= a.ncols) continue;   // uniform
       d4_t d;
 #pragma unroll
       for (int i = 0; i < 4; ++i) d[i] = Ys[rrow][16 * ct + l16 + 4 * i];
 #pragma unroll
-      for (int s4 = 0; s4 < 16; ++s4)
+      for (int s4 = 0; s4 < 4 * TM; ++s4)
         d = Mfma<double>::op(-ZW[4 * s4 + l16][16 * ct + m16], Vs[rrow][4 * s4 + l16], d);
       if (r < r_end) {
 #pragma unroll
@@ -250,9 +258,12 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
 hipError_t launch_thin_apply(ThinApplyArgs a, int num_cus, hipStream_t s) {
   if (a.mr <= 0 || a.ncols <= 0) return hipSuccess;
   if (a.b < 1 || a.b > 64 || a.ncols > 64) return hipErrorInvalidValue;
+  // Blocks and widths of at most 32 need the 2 x 2 corner of the tiles.
+  const void* fn = a.b <= 32 && a.ncols <= 32
+                       ? reinterpret_cast<const void*>(thin_apply_kernel<2>)
+                       : reinterpret_cast<const void*>(thin_apply_kernel<4>);
   int occ = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-      &occ, reinterpret_cast<const void*>(thin_apply_kernel), 256, 0);
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 256, 0);
   if (e != hipSuccess) return e;
   // About 64 rows per workgroup, at most one workgroup per compute unit that
   // can be resident (the workgroups wait on each other).
@@ -262,7 +273,7 @@ hipError_t launch_thin_apply(ThinApplyArgs a, int num_cus, hipStream_t s) {
   G = ceil_div(a.mr, a.rows_per_wg);
   if (occ < 1 || G > (int64_t)occ * num_cus) return hipErrorCooperativeLaunchTooLarge;
   void* params[] = {&a};
-  return launch_resident(reinterpret_cast<const void*>(thin_apply_kernel),
+  return launch_resident(fn,
                          dim3((unsigned)G), dim3(256), params, s);
 }
 
