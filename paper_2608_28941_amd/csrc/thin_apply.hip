@@ -49,42 +49,45 @@ __global__ __launch_bounds__(256) void thin_apply_kernel(ThinApplyArgs a) {
   const int PT = (min(a.b, 64) + 15) / 16, CT = (min(a.ncols, 64) + 15) / 16;
   const int NS = PT * CT * 256;
 
+  // The loops below read rows and columns of Tl, Vs and Ys below TD only.
+  constexpr int TD = 16 * TM;
   // T (leading b x b block, upper triangular) to LDS: all loads issued
   // before the first use (columns past b read column 0), entries outside the
   // triangle replaced by zero (a select: whatever the padding holds, even a
   // NaN, does not reach W).
   {
-    double tv[16];
+    constexpr int NTT = TD * TD / 256;
+    double tv[NTT];
 #pragma unroll
-    for (int it = 0; it < 16; ++it) {
+    for (int it = 0; it < NTT; ++it) {
       const int idx = t + 256 * it;
-      const int i = idx % 64, j = idx / 64;
+      const int i = idx % TD, j = idx / TD;
       tv[it] = a.Tm[i + (int64_t)(j < a.b ? j : 0) * a.ldt];
     }
 #pragma unroll
-    for (int it = 0; it < 16; ++it) {
+    for (int it = 0; it < NTT; ++it) {
       const int idx = t + 256 * it;
-      const int i = idx % 64, j = idx / 64;
+      const int i = idx % TD, j = idx / TD;
       Tl[i][j] = (i <= j && j < a.b) ? tv[it] : 0.0;
     }
   }
   // Rows [r0, r0 + 64) of V (reflectors < b) and Y (columns < ncols) to LDS,
-  // zero elsewhere: thread t loads row t % 64 of 16 columns, so every
-  // wavefront load reads 64 consecutive rows of one column.
+  // zero elsewhere up to column TD: thread t loads row t % 64 of TD / 4
+  // columns, so every wavefront load reads 64 consecutive rows of one column.
   auto stage = [&](int64_t r0) {
     const int rr = t % 64, c0 = t / 64;
     const int64_t r = r0 + rr;
     const bool ok = r < r_end;
     const int64_t rc = ok ? r : r_begin;   // in range; masked below
-    double vv[16], yy[16];
+    double vv[TD / 4], yy[TD / 4];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < TD / 4; ++i) {
       const int c = c0 + 4 * i;
       vv[i] = a.V[rc + (int64_t)(c < a.b ? c : 0) * a.ldv];
       yy[i] = a.Y[rc + (int64_t)(c < a.ncols ? c : 0) * a.ldy];
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < TD / 4; ++i) {
       const int c = c0 + 4 * i;
       Vs[rr][c] = (ok && c < a.b) ? vv[i] : 0.0;
       Ys[rr][c] = (ok && c < a.ncols) ? yy[i] : 0.0;
