@@ -148,6 +148,7 @@ struct rrf_plan {
   unsigned long long *red, *rowj, *gx, *tx;
   DevState* st;
   DevState* st_host;
+  DevState* st_mirror;   // st_host's device address (the finalisation's copy)
   int stop_mode, timing, panel_target;
   int log;                   // RRF_LOG=1: one stderr line per run, one per block
   int gram_fused_max;         // most workgroups of a Gram panel inside the update's launch
@@ -163,7 +164,7 @@ struct rrf_plan {
   double ms[RRF_NUM_STAGES], flops[RRF_NUM_STAGES], bytes[RRF_NUM_STAGES];
   int64_t launches[RRF_NUM_STAGES];
   std::vector<hipEvent_t> events;
-  hipEvent_t state_ev = nullptr;   // the run state's copy to the host has landed
+  hipEvent_t state_ev = nullptr;   // the launch holding a stop test has completed
   void* map_c = nullptr;           // subspace map: split partials and C
   size_t map_c_bytes = 0;
   std::vector<int> event_stage;
@@ -490,7 +491,7 @@ void set_finalize(rrf_plan* p, UpdateArgs<T>& u, int nparts, int block, int64_t 
   u.fin_epoch = next_epoch(p) + 1u;
   u.fin_nwg = nparts;
   FinalizeArgs& f = u.fin;
-  f.nparts = nparts; f.st = p->st; f.tt = p->trace_trail_d; f.ts = p->trace_sub_d;
+  f.nparts = nparts; f.st = p->st; f.mirror = p->st_mirror; f.tt = p->trace_trail_d; f.ts = p->trace_sub_d;
   f.block = block; f.k_after = k_after; f.k_cap = k_cap; f.mode = mode; f.tol = tol;
   f.init = init;
 }
@@ -957,7 +958,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     }
     if (!fin_in_update)
       RRF_LAUNCH(p, RRF_STAGE_FINALIZE, 0.0, 16.0 * nparts,
-                 launch_finalize(p->normpart, nparts, p->st, p->trace_trail_d,
+                 launch_finalize(p->normpart, nparts, p->st, p->st_mirror, p->trace_trail_d,
                                  p->trace_sub_d, at_end ? blk : -1, k_next, kcap,
                                  mode, tol, 0, s));
     if (!at_end) {
@@ -993,16 +994,14 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       next_panel = route_n >= 0;
     }
     if (la && more_likely && panel_ready) next_w = true;
-    if ((next_panel || next_w) && !p->state_ev) {
+    if (!p->state_ev) {
       he = hipEventCreateWithFlags(&p->state_ev, hipEventDisableTiming);
       if (he != hipSuccess) return hip_fail(he);
     }
-    he = hipMemcpyAsync(p->st_host, p->st, sizeof(DevState), hipMemcpyDeviceToHost, s);
+    // The stop test of this launch has written its decision into st_host;
+    // the event marks the launch's completion.
+    he = hipEventRecord(p->state_ev, s);
     if (he != hipSuccess) return hip_fail(he);
-    if (next_panel || next_w) {
-      he = hipEventRecord(p->state_ev, s);
-      if (he != hipSuccess) return hip_fail(he);
-    }
     if (next_w) {
       rrf_status rs = issue_w(k_next, b_next, Bws, ldb, true);
       if (rs != RRF_OK) return rs;
@@ -1028,7 +1027,7 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       RRF_LAUNCH(p, RRF_STAGE_PANEL, pfl, pby, run_panel(p, pn, route_n, shn, s));
       spec(RRF_STAGE_PANEL, k_next, pfl, pby + gby);
     }
-    he = (next_panel || next_w) ? hipEventSynchronize(p->state_ev) : hipStreamSynchronize(s);
+    he = hipEventSynchronize(p->state_ev);
     if (he != hipSuccess) return hip_fail(he);
     k = k_next;
     ++blk;
@@ -1459,8 +1458,11 @@ rrf_status plan_create(rrf_plan_t* plan, int dtype_bits, int64_t m_max, int64_t 
     ++counter;
     const char* f = std::getenv("RRF_FAULT_ALLOC");
     if (f && std::atoi(f) == counter) e = hipErrorOutOfMemory;
-    else e = hipHostMalloc((void**)&p->st_host, sizeof(DevState), 0);
+    else e = hipHostMalloc((void**)&p->st_host, sizeof(DevState),
+                           hipHostMallocMapped | hipHostMallocCoherent);
   }
+  // The stop test writes its decision straight into st_host.
+  if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&p->st_mirror, p->st_host, 0);
   if (e == hipSuccess) e = hipHostMalloc((void**)&p->groups_h, p->sz.groups, 0);
   if (e == hipSuccess) e = hipMemsetAsync(p->red, 0, p->sz.red, p->stream);
   if (e == hipSuccess) e = hipMemsetAsync(p->rowj, 0, p->sz.rowj, p->stream);

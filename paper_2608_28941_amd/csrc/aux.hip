@@ -41,11 +41,11 @@ __global__ void convert_kernel(const Ts* src, int64_t lds, Td* dst, int64_t ldd,
 }  // namespace
 
 hipError_t launch_finalize(const double* normpart, int nparts, DevState* st,
-                           double* trace_trail, double* trace_sub, int block,
+                           DevState* mirror, double* trace_trail, double* trace_sub, int block,
                            int64_t k_after, int64_t k_cap, int mode,
                            double tol, int init, hipStream_t s) {
   FinalizeArgs f{};
-  f.nparts = nparts; f.st = st; f.tt = trace_trail; f.ts = trace_sub; f.block = block;
+  f.nparts = nparts; f.st = st; f.mirror = mirror; f.tt = trace_trail; f.ts = trace_sub; f.block = block;
   f.k_after = k_after; f.k_cap = k_cap; f.mode = mode; f.tol = tol; f.init = init;
   hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(256), 0, s, normpart, f);
   return hipGetLastError();

@@ -86,6 +86,21 @@ __device__ __forceinline__ void finalize_state(const FinalizeArgs& f, double blk
       st->stop = st->nonfinite || werr;
     }
   }
+  // The host reads the decision from its pinned copy once the launch has
+  // completed (no copy in the stream).  A wait error recorded later in the
+  // same launch stays in *st and reaches the host with a later decision or
+  // an explicit state read.
+  if (DevState* h = f.mirror) {
+    h->E0 = st->E0;
+    h->sigma2 = st->sigma2;
+    h->E_trail = st->E_trail;
+    h->E_sub = st->E_sub;
+    h->stop = st->stop;
+    h->nonfinite = st->nonfinite;
+    h->barrier_err = werr;
+    h->spin_limit = st->spin_limit;
+    h->E_spec = st->E_spec;
+  }
 }
 
 // Finalize from plain partials (2 doubles per part).

@@ -58,6 +58,8 @@ struct DevState {
 struct FinalizeArgs {
   int nparts;
   DevState* st;
+  DevState* mirror;   // pinned host copy of *st, written with the decision
+                      // (device address; nullable)
   double* tt; double* ts;
   int block;
   int64_t k_after, k_cap;
@@ -335,7 +337,7 @@ hipError_t launch_subspace_map(const T* Qnew, int64_t ldqn, int64_t r_new, const
                                T* C, int nsplit, hipStream_t s);
 
 hipError_t launch_finalize(const double* normpart, int nparts, DevState* st,
-                           double* trace_trail, double* trace_sub, int block,
+                           DevState* mirror, double* trace_trail, double* trace_sub, int block,
                            int64_t k_after, int64_t k_cap, int mode,
                            double tol, int init, hipStream_t s);
 template <typename T>
