@@ -970,9 +970,10 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       ysplits = su;
       continue;
     }
-    // Work for the next block that does not depend on the stop test is
-    // queued behind the copy of the run state, and the host waits for the
-    // copy alone, so the device keeps working while the host reads the test:
+    // The stop test writes its decision into the pinned host state; the host
+    // waits on an event behind that launch alone, with the next block's work
+    // that does not depend on the test queued behind the event, so the
+    // device keeps working while the host reads the test:
     // without look-ahead the next block's gather and panel (they need only
     // the sample this update took), with look-ahead (the next panel is
     // already factored) its reduce and formW.  It is queued when the
