@@ -242,7 +242,7 @@ int red_splits(int64_t mr, int64_t n, int num_cus) {
   const int64_t col_wgs = ceil_div(n, kRedCols);
   int64_t s = ceil_div(4 * (int64_t)num_cus, std::max<int64_t>(col_wgs, 1));
   s = std::min<int64_t>(s, kMaxRedSplits);
-  s = std::min<int64_t>(s, std::max<int64_t>(1, mr / 256));
+  s = std::min<int64_t>(s, std::max<int64_t>(1, mr / kRedChunk));
   return (int)std::max<int64_t>(s, 1);
 }
 
