@@ -348,17 +348,20 @@ __device__ __forceinline__ void panel_gram_body(const GramPanelArgs& ga, const i
     // j + 1 after this step (removed from F).
     if (t < BP) {
       const int kk = t;
-      const double wv2 = L.top[j][kk] + scale * L.ujv[p][kk];
+      // Every read first: the only top entry written here, (kk, j) for
+      // kk < j, is none of the entries read (rows j and j + 1, and (kk, j)
+      // for kk > j), so no read waits for a write.
+      const int j1 = (j + 1 < BP) ? j + 1 : j;
+      const double tjk = L.top[j][kk], ujk = L.ujv[p][kk], tkj = L.top[kk][j];
+      const double xj1 = L.top[j1][j], yk = L.top[j1][kk];
+      const double wv2 = tjk + scale * ujk;
       const double cwk = (kk > j && kk < b) ? tau_j * wv2 * scale : 0.0;
       L.cw[kk] = cwk;
       if (kk < j) L.top[kk][j] = wv2;   // v_kk^T v_j, for T
-      L.xt[kk] = (kk > j && kk < b) ? L.top[kk][j] : 0.0;
+      L.xt[kk] = (kk > j && kk < b) ? tkj : 0.0;
       double zk = 0.0;
-      if (j + 1 < b && kk < b) {
-        const double xj1 = L.top[j + 1][j];
-        const double yk = L.top[j + 1][kk];
+      if (j + 1 < b && kk < b)
         zk = (kk > j) ? yk - cwk * xj1 : ((kk == j) ? scale * xj1 : yk);
-      }
       L.zv[kk] = zk;
       if (kk == j) {
         L.tau[j] = tau_j;
@@ -422,12 +425,16 @@ __device__ __forceinline__ void panel_gram_body(const GramPanelArgs& ga, const i
         for (int i = 0; i < BR; ++i) {
           const int r = BR * bi + i;
           if (r > j && r < b) {
+            // The row's entries are read together, then written (each entry
+            // belongs to one thread).
             const double xr = L.xt[r];
+            double tv[BC];
+#pragma unroll
+            for (int jj = 0; jj < BC; ++jj) tv[jj] = L.top[r][BC * bj + jj];
 #pragma unroll
             for (int jj = 0; jj < BC; ++jj) {
               const int c = BC * bj + jj;
-              const double tv = L.top[r][c];
-              L.top[r][c] = (c == j) ? scale * xr : tv - cwc[jj] * xr;
+              L.top[r][c] = (c == j) ? scale * xr : tv[jj] - cwc[jj] * xr;
             }
           }
         }
