@@ -643,12 +643,34 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
   bool panel_ready = false;  // the panel of this sub-block was factored by the last update
   bool stop = p->st_host->stop != 0;
   bool w_ready = false;      // W of this sub-block was formed at the end of the last one
+  bool w_gathered = false;   // ... together with its look-ahead gather
   double E_prev2 = 0.0;      // the stopping quantity one state read earlier
 
+  // The look-ahead gather of the sample S that the panel of sub-block
+  // kk + bb is factored from (sums of the split partials, slab rows from yo,
+  // ys splits, rows kk..m), as the look-ahead branch below issues it.  It
+  // needs only the update before sub-block kk, so it rides in the formW
+  // launch of sub-block kk.  False: no look-ahead panel follows.
+  auto la_gather = [&](int64_t kk, int64_t bb, int64_t yo, int ys, GatherArgs<T>* g,
+                       double* gby) -> bool {
+    const int64_t bn = sub_width(kk + bb);
+    if (!la || bn <= 0) return false;
+    const int64_t mpp = m - kk;
+    PanelShape shn;
+    if (!la_shape(mpp - bb, bn, &shn)) return false;
+    g->P = Yp + yo; g->ldp = ldb; g->split_stride = ldb * 64; g->nsplit = ys;
+    g->m = mpp; g->b = (int)bn; g->bp = pad16(bn); g->rows_pad = bb + shn.rows_pad;
+    g->Y = p->Ysum; g->ldy = p->sz.ldysum;
+    *gby = e * mpp * bn * ys + 8.0 * mpp * bn;
+    return true;
+  };
   // Z = V^T B[kk:m, :] and W = T^T Z of the sub-block at kk (width bb),
   // from the rows kk..m of sx; speculative when queued ahead of a stop test.
+  // ga (nullable): the look-ahead gather for sub-block kk + bb, in the same
+  // launch as formW (gby: its bytes).
   auto issue_w = [&](int64_t kk, int64_t bb, const T* sx, int64_t ldsx,
-                     bool speculative) -> rrf_status {
+                     bool speculative, const GatherArgs<T>* ga = nullptr,
+                     double gby = 0.0) -> rrf_status {
     const int64_t mpp = m - kk;
     const int bpp = pad16(bb);
     const int sr0 = red_splits(mpp, n, p->num_cus);
@@ -665,12 +687,14 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     fa.Tm = Tm + kk * kTLd; fa.ldt = kTLd; fa.W = (T*)p->W; fa.n = n; fa.bp = bpp;
     fa.trans = 1;
     fa.b = (int)bb;
+    if (ga) fa.g = *ga;
     const double wfl = 1.0 * n * bb * bb, wby = e * n * bb * (sr + 1);
-    RRF_LAUNCH(p, RRF_STAGE_FORMW, wfl, wby, launch_formw<T>(fa, s));
+    RRF_LAUNCH(p, RRF_STAGE_FORMW, wfl, wby + (ga ? gby : 0.0), launch_formw<T>(fa, s));
     if (speculative) {
       spec(RRF_STAGE_REDUCE, kk, rfl, rby);
       spec(RRF_STAGE_FORMW, kk, wfl, wby);
     }
+    if (ga) spec(RRF_STAGE_FORMW, kk + bb, 0.0, gby);
     return RRF_OK;
   };
   auto panel_flops = [](double mr, double bb) {
@@ -834,10 +858,15 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
 
     // Z = V_i^T B[k:m, :], W = T_i^T Z (unless queued at the end of the last
     // block).
+    bool gathered = false;     // the look-ahead gather rode in formW's launch
     if (w_ready) {
       w_ready = false;
+      gathered = w_gathered;
     } else {
-      rrf_status rs = issue_w(k, bi, src, lsrc, false);
+      GatherArgs<T> ga{};
+      double gby = 0.0;
+      gathered = la_gather(k, bi, yoff, ysplits, &ga, &gby);
+      rrf_status rs = issue_w(k, bi, src, lsrc, false, gathered ? &ga : nullptr, gby);
       if (rs != RRF_OK) return rs;
     }
 
@@ -851,12 +880,14 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       const int bpn = pad16(b_next);
       PanelShape shn;
       if (!la_shape(mpn, b_next, &shn)) return RRF_ERR_SHAPE;
-      const double gby = e * mp * b_next * ysplits + 8.0 * mp * b_next;
-      RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, gby,
-                 launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
-                                        (int)b_next, bpn, bi + shn.rows_pad,
-                                        p->Ysum, p->sz.ldysum, s));
-      spec(RRF_STAGE_PANEL, k_next, 0.0, gby);
+      if (!gathered) {
+        const double gby = e * mp * b_next * ysplits + 8.0 * mp * b_next;
+        RRF_LAUNCH(p, RRF_STAGE_PANEL, 0.0, gby,
+                   launch_gather_panel<T>(Yp + yoff, ldb, ldb * 64, ysplits, mp,
+                                          (int)b_next, bpn, bi + shn.rows_pad,
+                                          p->Ysum, p->sz.ldysum, s));
+        spec(RRF_STAGE_PANEL, k_next, 0.0, gby);
+      }
       ThinApplyArgs ta{};
       ta.V = V + k + k * ldb; ta.ldv = ldb;
       ta.Tm = Tm + k * kTLd; ta.ldt = kTLd; ta.b = (int)bi; ta.trans = 1;
@@ -1004,7 +1035,12 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
     he = hipEventRecord(p->state_ev, s);
     if (he != hipSuccess) return hip_fail(he);
     if (next_w) {
-      rrf_status rs = issue_w(k_next, b_next, Bws, ldb, true);
+      // Its look-ahead gather reads the partials this update wrote (slab
+      // rows from bi, su splits).
+      GatherArgs<T> ga{};
+      double gby = 0.0;
+      w_gathered = la_gather(k_next, b_next, bi, su, &ga, &gby);
+      rrf_status rs = issue_w(k_next, b_next, Bws, ldb, true, w_gathered ? &ga : nullptr, gby);
       if (rs != RRF_OK) return rs;
     }
     if (next_panel) {

@@ -2,6 +2,7 @@
 // (a grid of mutually waiting workgroups; the workgroup body is in
 // panel_body.h), the gather of the sampled panel and the launchers.
 
+#include "gather_body.h"
 #include "panel_body.h"
 
 namespace rrf {
@@ -18,12 +19,8 @@ __global__ void gather_panel_kernel(const T* P, int64_t ldp, int64_t split_strid
                                     int64_t rows_pad, double* Y, int64_t ldy) {
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= rows_pad) return;
-  for (int k = blockIdx.y; k < bp; k += gridDim.y) {
-    double v = 0.0;
-    if (r < m && k < b)
-      for (int s = 0; s < nsplit; ++s) v += (double)P[s * split_stride + r + k * ldp];
-    Y[r + k * ldy] = v;
-  }
+  const GatherArgs<T> g{P, ldp, split_stride, nsplit, m, b, bp, rows_pad, Y, ldy};
+  for (int k = blockIdx.y; k < bp; k += gridDim.y) gather_entry(g, r, k);
 }
 
 template <int BP, int RPT>

@@ -101,6 +101,16 @@ struct ReduceArgs {
   int64_t rows_per_split;
 };
 
+// The gathered sample: Y[r + k ldy] = sum over the split partials
+// P[s split_stride + r + k ldp] in split order (binary64), for rows < m and
+// columns < b, zero elsewhere up to rows_pad x bp (gather_body.h).
+template <typename T>
+struct GatherArgs {
+  const T* P; int64_t ldp, split_stride; int nsplit;
+  int64_t m; int b, bp; int64_t rows_pad;
+  double* Y; int64_t ldy;
+};
+
 template <typename T>
 struct FormWArgs {
   const T* Z; int nsplit; int64_t split_stride;
@@ -109,6 +119,11 @@ struct FormWArgs {
   int64_t n; int bp;
   int b;                       // block width: T rows / columns >= b are ignored
   int trans;                   // 1: W = T^T Z,  0: W = T Z
+  // Optional (g.nsplit > 0, bp <= 64): extra workgroups of the same launch
+  // gather the look-ahead sample (the inputs of both come from the last
+  // update); nfw, the formW workgroups, is set by the launcher.
+  GatherArgs<T> g;
+  int nfw;
 };
 
 struct PanelArgs {

@@ -24,6 +24,7 @@
 
 #include <type_traits>
 
+#include "gather_body.h"
 #include "mfma.h"
 #include "rrf_internal.h"
 #include "update_body.h"
@@ -179,9 +180,19 @@ __global__ __launch_bounds__(256, 2) void reduce_kernel(ReduceArgs<T> a) {
 // formW: W[c * BP + p] = (T^T z_c)_p (trans) or (T z_c)_p, z_c = sum_s Z_s[c]
 // Only the leading b x b block of T is used (the padding columns of a stored
 // block may already hold the next block's T), so W rows >= b are zero.
+// Workgroups past the first a.nfw gather the look-ahead sample instead (one
+// per 256 rows of one column, as the gather kernel).
 // ---------------------------------------------------------------------------
 template <typename T, int BP>
 __global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
+  if ((int)blockIdx.x >= a.nfw) {   // uniform
+    const int64_t gi = (int64_t)blockIdx.x - a.nfw;
+    const int64_t nrb = (a.g.rows_pad + 255) / 256;
+    const int k = (int)(gi / nrb);
+    const int64_t r = (gi % nrb) * 256 + threadIdx.x;
+    if (r < a.g.rows_pad && k < a.g.bp) gather_entry(a.g, r, k);
+    return;
+  }
   constexpr int CPB = 256 / BP;
   constexpr int NT = (BP * BP) / 256;
   constexpr int ZB = 8;                // split partials loaded together
@@ -210,7 +221,7 @@ __global__ __launch_bounds__(256) void formw_kernel(FormWArgs<T> a) {
   // can stage whole chunks without predicates.
   const int64_t n_pad = (a.n + kUpdChunk - 1) / kUpdChunk * kUpdChunk;
   for (int64_t c0 = (int64_t)blockIdx.x * CPB; c0 < n_pad;
-       c0 += (int64_t)gridDim.x * CPB) {
+       c0 += (int64_t)a.nfw * CPB) {
     __syncthreads();
     const int64_t c = c0 + cl;
     // z_c = sum over the splits in split order, ZB loads in flight at a time
@@ -432,11 +443,21 @@ hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s) {
   // workgroups, each over more columns, keep that re-read small.
   const int64_t cap = a.bp == 128 ? 256 : 2048;
   if (blocks > cap) blocks = cap;
-  dim3 grid((unsigned)blocks);
+  // The gather's workgroups follow formW's.
+  FormWArgs<T> a2 = a;
+  a2.nfw = (int)blocks;
+  int64_t gblocks = 0;
+  if (a.g.nsplit > 0 && a.g.rows_pad > 0) {
+    if (a.bp > 64 || a.g.bp < 1) return hipErrorInvalidValue;
+    gblocks = ceil_div(a.g.rows_pad, 256) * a.g.bp;
+  } else {
+    a2.g.nsplit = 0;
+  }
+  dim3 grid((unsigned)(blocks + gblocks));
   switch (a.bp) {
-    case 16: hipLaunchKernelGGL((formw_kernel<T, 16>), grid, dim3(256), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((formw_kernel<T, 32>), grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((formw_kernel<T, 64>), grid, dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((formw_kernel<T, 16>), grid, dim3(256), 0, s, a2); break;
+    case 32: hipLaunchKernelGGL((formw_kernel<T, 32>), grid, dim3(256), 0, s, a2); break;
+    case 64: hipLaunchKernelGGL((formw_kernel<T, 64>), grid, dim3(256), 0, s, a2); break;
     case 128:
       if constexpr (std::is_same<T, double>::value) {
         if (!a.trans) {
@@ -456,7 +477,7 @@ hipError_t launch_formw(const FormWArgs<T>& a, hipStream_t s) {
                                dim3(256), 0, s, a);
           break;
         }
-        hipLaunchKernelGGL((formw_kernel<T, 128>), grid, dim3(256), 0, s, a);
+        hipLaunchKernelGGL((formw_kernel<T, 128>), grid, dim3(256), 0, s, a2);
         break;
       }
       return hipErrorInvalidValue;
