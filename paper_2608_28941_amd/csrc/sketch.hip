@@ -151,6 +151,36 @@ __global__ __launch_bounds__(256) void sketch_kernel(
   }
 }
 
+// Row-major output (col_stride 1): lanes along the columns, so that a
+// wavefront store covers 64 consecutive columns of one row; each thread makes
+// the four rows of one Philox block, as above (same blocks, same values).
+// Wavefront w of a workgroup takes row quads blockIdx.x * 4 + w + 4 gridDim.x i.
+template <typename T>
+__global__ __launch_bounds__(256) void sketch_rows_kernel(
+    uint64_t seed, int64_t n, int64_t n_pad, int64_t col0, int64_t ncols,
+    T* out, int64_t row_stride) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t j = (int64_t)blockIdx.y * 64 + lane;
+  if (j >= ncols) return;
+  const int64_t nq = (n_pad + 3) / 4;
+  for (int64_t q = (int64_t)blockIdx.x * 4 + wv; q < nq; q += (int64_t)gridDim.x * 4) {
+    T v[4] = {T(0), T(0), T(0), T(0)};
+    if (4 * q < n) {
+      uint64_t w[4];
+      philox4x64_10((uint64_t)q, (uint64_t)(col0 + j), 0ull, 0ull, seed, 0ull, w);
+      double z[4];
+      box_muller(w[0], w[1], &z[0], &z[1]);
+      box_muller(w[2], w[3], &z[2], &z[3]);
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (4 * q + t < n) v[t] = (T)z[t];
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      if (4 * q + t < n_pad) out[(4 * q + t) * row_stride + j] = v[t];
+  }
+}
+
 }  // namespace
 
 template <typename T>
@@ -160,6 +190,13 @@ hipError_t launch_sketch(uint64_t seed, int64_t n, int64_t n_pad, int64_t col0,
   if (n <= 0 || ncols <= 0) return hipSuccess;
   if (n_pad < n) n_pad = n;
   const int64_t nq = (n_pad + 3) / 4;
+  if (col_stride == 1 && ceil_div(ncols, 64) <= 65535) {
+    const dim3 rgrid((unsigned)std::min<int64_t>(ceil_div(nq, 4), 4096),
+                     (unsigned)ceil_div(ncols, 64));
+    hipLaunchKernelGGL(sketch_rows_kernel<T>, rgrid, dim3(256), 0, s, seed, n, n_pad,
+                       col0, ncols, out, row_stride);
+    return hipGetLastError();
+  }
   dim3 grid((unsigned)ceil_div(nq, 256), (unsigned)(ncols < 65535 ? ncols : 65535));
   hipLaunchKernelGGL(sketch_kernel<T>, grid, dim3(256), 0, s, seed, n, n_pad,
                      col0, ncols, out, row_stride, col_stride);
