@@ -1133,8 +1133,8 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
       }
     }
     if (ngroups > 0) {
-      // Row splits of the Gram sums: about 256 rows each, within the partial
-      // buffer (ngroups x (nsplit + 1) matrices of kGroupMax^2).
+      // Row splits of the Gram sums, within the partial buffer (ngroups x
+      // (nsplit + 1) matrices of kGroupMax^2).
       const int64_t ent = (int64_t)kGroupMax * kGroupMax;
       const int64_t cap = (int64_t)(p->sz.Zpart / 8) / (ent * ngroups) - 1;
       if (cap < 1) {
@@ -1157,7 +1157,12 @@ rrf_status run_impl(rrf_plan* p, const T* A, int64_t m, int64_t n, int64_t lda,
         ga.V = V; ga.ldv = ldb; ga.m = m;
         ga.Tm = Tm; ga.ldt = kTLd; ga.Tg = p->Tp; ga.ldg = kGroupMax;
         ga.part = (double*)p->Zpart;
-        ga.nsplit = (int)std::max<int64_t>(1, std::min<int64_t>({ceil_div(gram_rows, 256), 64, cap}));
+        // About two workgroups per compute unit over all groups (each split is
+        // a chain of 32-row chunks), splits of at least 256 rows.
+        ga.nsplit = (int)std::max<int64_t>(
+            1, std::min<int64_t>({ceil_div(gram_rows, 256),
+                                  std::max<int64_t>(64, ceil_div(2 * (int64_t)p->num_cus, ngroups)),
+                                  cap}));
         RRF_LAUNCH(p, RRF_STAGE_ORGQR, 2.0 * gram_rows * ent * ngroups,
                    8.0 * gram_rows * kGroupMax * ngroups, launch_orgqr_groups(ga, s));
       }
